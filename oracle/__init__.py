@@ -1,0 +1,39 @@
+"""Reference oracle for the AutoLoCo synchronisation round — TEST INFRASTRUCTURE.
+
+A plain, slow, CPU-only evaluation of what one synchronisation round computes,
+written from the paper (arxiv 2609.36662, "AutoLoCo: Communication Efficient
+Distributed LLM Training via Adaptive Synchronization") in float64 and exact
+rational arithmetic.  It exists to check the GPU library against; it is not
+part of the library.
+
+Only the test suite, the smoke check of the package entry file and the CPU
+baseline leg of the benchmark may import or run anything in this package.  It
+shares no code with the HIP/C++ library: it includes no header of it, loads no
+binary of it and reuses none of its constants or helpers.
+
+Modules
+  round       — pseudo-gradients, their mean, local-drift energy D and
+                aggregation coherence C (Sec. "Adaptive Interval Selection",
+                eq. adaptive-h-core-diagnostics; App. C.1), the corrected
+                Nesterov outer step (eq. autoloco-corrected-nesterov) and the
+                replica reset (Alg. "AutoLoCo outer interval").
+  exact       — the same round in ``fractions.Fraction`` arithmetic for tiny
+                inputs (brute-force pin of ``round``).
+  correction  — the inner learning-rate schedule, learning-rate masses and the
+                Outer Optimizer Correction (eqs. outer-correction-ratio,
+                normalized-pseudo-gradient, adjusted-outer-learning-rate;
+                App. B.2-B.4).
+  controller  — the adaptive interval controller and token mapper (Sec.
+                "Adaptive Interval Selection"; App. A).
+
+Parity unpinned (no value printed by the paper and no closed form fixes them;
+each is one reading of a point the paper leaves open):
+  * the robust scale floor and MAD consistency factor used for z_max,
+  * the coefficient of the log-space EMA of the reference diagnostics,
+  * tie-breaking of reductions and geometric midpoints,
+  * the count of severe/invalid intervals that triggers the H_min fallback,
+  * the rejected-horizon bound and reduction paths beyond their printed
+    constants.
+The adaptive-interval controller is otherwise pinned by the executed interval
+sequence the paper prints for its C4 run (App. F.2).
+"""
