@@ -1,0 +1,257 @@
+#!/usr/bin/env python3
+"""Benchmark of one fused AutoLoCo synchronisation round on one MI355X.
+
+A step is one whole round through the C ABI: autoloco_outer_step with fused
+statistics and replica reset (pseudo-gradients, their mean, D/C diagnostics,
+corrected Nesterov step, reset of every replica), including the copy of the
+2K+1 sums to the host.  The default workload is the 1.1B-parameter
+Llama-style model (22 layers, d=2048, FFN 5632, vocab 32000, 4 KV heads) with
+K=8 fp32 replicas, inputs resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps 20] [--warmup 3] [--workload llama-1.1b]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sync-round params/s and achieved HBM GB/s (% of peak), 1.1B params K=8"
+PEAK_HBM_GBS = 8000.0
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_36662_amd", "csrc", f)
+                  for f in ("round_kernels.hpp", "round_inst.hip")]
+
+# name -> (shape, K, replica dtype, recipe, selected horizon, base horizon)
+WORKLOADS = {
+    "llama-1.1b": ("llama-1.1b", 8, "f32", "mixed", 750, 500),
+    "gpt2-small": ("gpt2-small", 8, "f32", "spread1e-3", 750, 500),
+    "llama-3b-bf16": ("llama-3b", 8, "bf16", "mixed", 750, 500),
+    "llama-7b": ("llama-7b", 4, "f32", "mixed", 750, 500),
+    "tiny": (None, 4, "f32", "mixed", 75, 50),
+}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(tag: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    kernel, if it was taken on the current kernel source; else None."""
+    path = os.path.join(PROFILE_DIR, f"{tag}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(sample, coeffs, seconds: float, desc: str):
+    """The float64 oracle, as it stands, on a bounded sample of the workload."""
+    import numpy as np
+    from oracle import round as orr
+    th, mom, reps, rdt = sample
+    n = th.shape[0]
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        res = orr.sync_round(th, mom, reps, coeffs.mu, coeffs.eta_out, coeffs.rho, bool(coeffs.normalize),
+                             1e-12)
+        orr.reset_replicas(res.theta, len(reps), rdt)
+        done += n
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    del np
+    return {"value": done / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": f"{desc}: first {n:,} parameters of every buffer, round repeated "
+                      f"{done // n}x over {dt:.1f} s (numpy float64, one thread)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama-1.1b", choices=sorted(WORKLOADS))
+    ap.add_argument("--grid", type=int, default=0, help="cap on workgroups (0 = library default)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 22)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true")
+    ap.add_argument("--perturbed", type=int, default=3, help="extra rounds on freshly drawn replicas")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the round keeps all K replicas on one device and has no "
+              f"multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift, shapes
+
+    shape_name, k, rdt, recipe_name, h_sel, h_base = WORKLOADS[args.workload]
+    n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    recipe = drift.MIXED if recipe_name == "mixed" else drift.spread_recipe(1e-3)
+    tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
+    s_r = 4 if rdt == "f32" else 2
+    bytes_per_round = n * (2 * k * s_r + 16)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # Outer coefficients from the library's own schedule preview and correction.
+    sched = al.make_schedule()
+    lam = al.autoloco_lr_mass(sched, 20_000, h_sel)
+    lam_b = al.autoloco_lr_mass(sched, 20_000, h_base)
+    coeffs = al.autoloco_outer_correction(al.make_outer_cfg(), lam, lam_b)
+
+    log(f"workload {args.workload}: n={n:,} K={k} replicas={rdt} bytes/round={bytes_per_round/1e9:.3f} GB")
+    t = time.perf_counter()
+    inp = drift.make_round_inputs(n, k, seed=42, recipe=recipe, replica_dtype=tdtype, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs generated in {time.perf_counter() - t:.1f} s")
+
+    sample = None
+    if not args.no_cpu_baseline:
+        s = min(n, args.cpu_sample)
+        import numpy as np
+        def host(tn):
+            x = tn[:s].cpu()
+            return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
+        sample = (host(inp.theta), host(inp.momentum), [host(r) for r in inp.replicas], rdt)
+
+    ctx = al.autoloco_create(0)
+    if args.grid:
+        al.autoloco_set_grid_limit(ctx, args.grid)
+    blocks, threads = al.autoloco_launch_shape(ctx, n, al.F32 if rdt == "f32" else al.BF16)
+    al.autoloco_set_timing(ctx, True)
+    flags = al.FUSE_STATS | al.FUSE_RESET
+
+    def one_round():
+        st = al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, coeffs, flags, 1e-12)
+        return st, al.autoloco_last_kernel_ms(ctx)
+
+    first_stats = None
+    for i in range(args.warmup):
+        st, _ = one_round()
+        if i == 0:
+            first_stats = st.as_dict()
+        drift.fill_replicas(inp, seed=43 + i, recipe=recipe)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} rounds); grid {blocks} x {threads}")
+
+    kernel_ms = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        _, ms = one_round()
+        kernel_ms.append(ms)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    log(f"timed {args.steps} rounds: {ms_per_step:.3f} ms/round wall, kernel mean "
+        f"{statistics.mean(kernel_ms):.3f} ms")
+
+    perturbed_ms = []
+    for i in range(args.perturbed):
+        drift.fill_replicas(inp, seed=1000 + i, recipe=recipe)
+        torch.cuda.synchronize()
+        _, ms = one_round()
+        perturbed_ms.append(ms)
+    if perturbed_ms:
+        log(f"rounds on freshly drawn replicas: kernel {statistics.median(perturbed_ms):.3f} ms (median)")
+
+    ceiling = None
+    if not args.no_ceiling:
+        nbytes = 4 << 30
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        times = []
+        for _ in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dst.copy_(src)
+            e1.record()
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1))
+        ceiling = 2 * nbytes / (statistics.median(times[1:]) * 1e-3) / 1e9
+        del src, dst
+        log(f"device-to-device copy of 4 GiB: {ceiling:.0f} GB/s")
+
+    ctx.close()
+    mean_ms = statistics.mean(kernel_ms)
+    achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
+    tag = f"round_{rdt}_k{k}_{args.workload}"
+    traffic = committed_traffic(tag)
+
+    cpu = None
+    if sample is not None:
+        log("timing the oracle on the CPU sample")
+        cpu = cpu_baseline(sample, coeffs, args.cpu_seconds, f"{args.workload} K={k} {rdt}")
+
+    out = {
+        "metric": METRIC,
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if rdt == "f32" else "f32 (bf16 replicas)",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {n:,} parameters as one flat arena per buffer, K={k} "
+                        f"{rdt} replicas, fp32 theta and momentum, fused stats + Nesterov + reset",
+            "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
+            "grid": [blocks, threads], "h_selected": h_sel, "h_base": h_base,
+            "rho": coeffs.rho, "mu": coeffs.mu, "eta_out": coeffs.eta_out,
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+        },
+        "kernel_ms_mean": mean_ms,
+        "kernel_ms_min": min(kernel_ms),
+        "kernel_ms_perturbed_median": statistics.median(perturbed_ms) if perturbed_ms else None,
+        "copy_ceiling_gbs": ceiling,
+        "first_round_stats": {k2: first_stats[k2] for k2 in ("D", "C", "disagreement", "finite")}
+        if first_stats else None,
+        "cpu_baseline": cpu,
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

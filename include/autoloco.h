@@ -1,0 +1,292 @@
+/*
+ * autoloco.h — C ABI of the AutoLoCo synchronisation-round library for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * One synchronisation round of AutoLoCo (arxiv 2609.36662, "AutoLoCo:
+ * Communication Efficient Distributed LLM Training via Adaptive
+ * Synchronization") on one GPU that holds all K worker replicas:
+ *
+ *   Delta_k   = theta - theta_k                       pseudo-gradient of worker k
+ *   Delta_bar = (1/K) sum_k Delta_k                   the synchronised average
+ *   D = (1/K) sum_k ||Delta_k||^2                     local-drift energy
+ *   C = K ||Delta_bar||^2 / (D + eps)                 aggregation coherence
+ *   Delta_tilde = Delta_bar / rho  (if normalising)   normalised pseudo-gradient
+ *   v' = mu v + Delta_tilde;  d = Delta_tilde + mu v';  theta' = theta - eta d
+ *   theta_k <- theta'                                 every worker restarts from theta'
+ *
+ * (Sec. "Adaptive Interval Selection", eq. adaptive-h-core-diagnostics;
+ * Sec. "Outer Optimizer Correction", eqs. normalized-pseudo-gradient and
+ * autoloco-corrected-nesterov; Alg. "AutoLoCo outer interval"; App. C.1 for
+ * the endpoint disagreement.)  The paper writes the worker count as N; this
+ * interface calls it k and uses n for the number of parameters.
+ *
+ * Device calls run on the HIP stream bound to the context.  Host-only calls
+ * (schedule, correction, controller) touch no device.
+ *
+ * Conventions for every call:
+ *   - Return value: AUTOLOCO_OK or a negative autoloco_status.  No call throws,
+ *     aborts or exits.  When argument validation fails, no device work is
+ *     launched and the outputs are left untouched; autoloco_last_error()
+ *     describes the failure.
+ *   - Ownership: the caller owns every buffer it passes (device or host) and
+ *     keeps it alive until the call's device work has finished.  The library
+ *     owns only the context's scratch memory.
+ *   - Device buffers are flat, contiguous arrays of n elements, 16-byte
+ *     aligned, and must not overlap one another.
+ *   - Non-finite values in the data are not an error: they propagate through
+ *     the update and are reported as finite = 0 in the statistics.
+ */
+#ifndef AUTOLOCO_H
+#define AUTOLOCO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Largest worker count: the paper runs 4, 8 and 16 workers. */
+#define AUTOLOCO_MAX_K 16
+
+typedef enum {
+    AUTOLOCO_OK = 0,
+    AUTOLOCO_E_INVALID = -1, /* null pointer, k or n out of range, unknown dtype or flag */
+    AUTOLOCO_E_ALIGN = -2,   /* a device pointer is not 16-byte aligned */
+    AUTOLOCO_E_ALIAS = -3,   /* two device buffers overlap */
+    AUTOLOCO_E_DEVICE = -4,  /* the HIP runtime reported an error */
+    AUTOLOCO_E_NOMEM = -5,   /* an allocation failed */
+    AUTOLOCO_E_STATE = -6    /* call out of order (e.g. controller after its budget) */
+} autoloco_status;
+
+typedef enum { AUTOLOCO_F32 = 0, AUTOLOCO_BF16 = 1 } autoloco_dtype;
+
+/* Text of a status code (static storage). */
+const char* autoloco_status_string(int status);
+
+/* ------------------------------------------------------------------------ */
+/* Context                                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* A context binds one device and one HIP stream and owns the scratch memory of
+ * the two-stage statistics reduction (per-block fp64 partial sums, a block
+ * counter and the final sums) plus a pinned host buffer for them.  One context
+ * serves one stream; calls on one context must not overlap.
+ *   device: HIP device ordinal.  stream: a hipStream_t of that device, or NULL
+ *   for the default stream.  *out receives the context.
+ * Errors: E_INVALID (null out, bad ordinal), E_DEVICE, E_NOMEM. */
+typedef struct autoloco_ctx autoloco_ctx;
+int autoloco_create(int device, void* stream, autoloco_ctx** out);
+void autoloco_destroy(autoloco_ctx* ctx);
+/* Message of the last failed call on ctx ("" if none).  Valid until the next call. */
+const char* autoloco_last_error(const autoloco_ctx* ctx);
+
+/* Record HIP events around every round kernel launched through ctx (on the
+ * context's stream) so that autoloco_last_kernel_ms() can report the device
+ * time of the most recent one.  Off by default. */
+int autoloco_set_timing(autoloco_ctx* ctx, int enable);
+/* Device milliseconds of the last timed launch; waits for it to finish. */
+int autoloco_last_kernel_ms(autoloco_ctx* ctx, float* ms);
+/* Cap on the number of workgroups of the streaming kernels (0 = the default,
+ * a fixed multiple of the device's compute units).  The statistics are
+ * bit-identical between runs with the same n, k and cap. */
+int autoloco_set_grid_limit(autoloco_ctx* ctx, int max_blocks);
+/* Workgroups and threads per workgroup a round over n parameters uses. */
+int autoloco_launch_shape(const autoloco_ctx* ctx, int64_t n, int32_t replica_dtype,
+                          int32_t* blocks, int32_t* threads);
+
+/* ------------------------------------------------------------------------ */
+/* Device buffers of one round                                               */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t n;             /* parameters per buffer, n >= 0 */
+    int32_t k;             /* worker replicas, 1..AUTOLOCO_MAX_K */
+    int32_t replica_dtype; /* autoloco_dtype of every replica */
+    float* theta;          /* [n] fp32: synchronised parameters theta_t (in/out) */
+    float* momentum;       /* [n] fp32: outer momentum v (in/out); unused by stats/reset */
+    void* replicas[AUTOLOCO_MAX_K]; /* k x [n] worker endpoints theta_k (read; written by a reset) */
+} autoloco_buffers;
+
+/* Sums over all n parameters and the diagnostics derived from them. */
+typedef struct {
+    double sq_norm[AUTOLOCO_MAX_K]; /* ||Delta_k||^2 */
+    double sq_dev[AUTOLOCO_MAX_K];  /* ||Delta_k - Delta_bar||^2 */
+    double sq_mean;                 /* ||Delta_bar||^2 */
+    double D;                       /* (1/k) sum_k sq_norm[k] */
+    double C;                       /* k sq_mean / (D + eps) */
+    double disagreement;            /* (1/k) sum_k sq_dev[k]  (= D - sq_mean, App. C.1) */
+    int32_t finite;                 /* 1 if every value above is finite */
+    int32_t k;
+} autoloco_stats;
+
+/* Coefficients of one corrected Nesterov step (see autoloco_outer_correction). */
+typedef struct {
+    double mu;         /* momentum retention mu_t */
+    double eta_out;    /* outer learning rate eta_t */
+    double rho;        /* interval ratio rho_t >= 1 */
+    double kappa;      /* bounded outer-step scale (reported; not used by the step) */
+    int32_t normalize; /* 1: Delta_tilde = Delta_bar / rho; 0: Delta_tilde = Delta_bar */
+} autoloco_outer_coeffs;
+
+#define AUTOLOCO_FUSE_STATS 1u /* also compute the round statistics of theta_t */
+#define AUTOLOCO_FUSE_RESET 2u /* also write theta_{t+1} into every replica */
+
+/* Statistics of one round (eq. adaptive-h-core-diagnostics; App. C.1):
+ * reads theta and the k replicas once, writes nothing but *out.  Blocks until
+ * the sums are on the host.  eps >= 0 is the constant in C.  Stats of the same
+ * buffers are bit-identical from run to run (fixed reduction order).
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_round_stats(autoloco_ctx* ctx, const autoloco_buffers* bufs, double eps,
+                         autoloco_stats* out);
+
+/* Corrected Nesterov outer step (eq. autoloco-corrected-nesterov, with the
+ * normalisation of eq. normalized-pseudo-gradient) in one pass over the
+ * buffers: theta and momentum are updated in place from theta_t, v_{t-1} and
+ * Delta_bar.  With AUTOLOCO_FUSE_STATS the statistics of theta_t are computed
+ * in the same pass (out required; the call then blocks until they are on the
+ * host).  With AUTOLOCO_FUSE_RESET every replica is overwritten with
+ * theta_{t+1} (bf16 replicas: rounded to nearest even), as each worker starts
+ * the next interval from the synchronised parameters (Alg. "AutoLoCo outer
+ * interval").  Without FUSE_STATS the call is asynchronous on the stream.
+ * The coefficients are applied in fp32 (mu, eta_out and 1/rho rounded once).
+ * Errors: E_INVALID (incl. unknown flags, null out with FUSE_STATS, null
+ * momentum), E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_outer_step(autoloco_ctx* ctx, const autoloco_buffers* bufs,
+                        const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
+                        autoloco_stats* out);
+
+/* Replica reset alone: theta_k <- theta for every replica (Alg. "AutoLoCo
+ * outer interval", start of the local loop).  Asynchronous on the stream.
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_broadcast_reset(autoloco_ctx* ctx, const autoloco_buffers* bufs);
+
+/* ------------------------------------------------------------------------ */
+/* Host-only scalar routines                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Inner learning-rate schedule: linear warm-up then cosine decay, the recipe
+ * of Table "Training settings".  eta(s) = peak (s+1)/warmup for s < warmup,
+ * else min_lr + (peak - min_lr)(1 + cos(pi min(1, (s - warmup)/(total - warmup))))/2,
+ * with s the 0-based global inner step. */
+typedef struct {
+    double peak, min_lr;
+    int64_t warmup, total;
+} autoloco_schedule;
+double autoloco_inner_lr(const autoloco_schedule* sched, int64_t step);
+
+/* Learning-rate mass sum_{h=1..steps} eta(start_step + h - 1): the exact
+ * scheduler preview of eq. app-outer-correction-lr-masses.  Returns NaN for a
+ * null schedule or negative arguments. */
+double autoloco_lr_mass(const autoloco_schedule* sched, int64_t start_step, int64_t steps);
+
+/* Outer Optimizer Correction (eqs. outer-correction-ratio,
+ * adjusted-outer-learning-rate; App. B.2-B.4):
+ *   rho = max(lambda_sel / (lambda_base + eps), 1), mu = clip(mu_base^rho, mu_min, mu_max),
+ *   kappa = min(rho, kappa_max), eta_out = eta_base kappa (1 - mu)/(1 - mu_base).
+ * Errors: E_INVALID (null pointers, non-finite masses, mu_base outside (0,1),
+ * mu_min > mu_max, kappa_max < 1). */
+typedef struct {
+    double eta_base, mu_base, mu_min, mu_max, kappa_max, eps;
+    int32_t normalize;
+} autoloco_outer_cfg;
+int autoloco_outer_correction(const autoloco_outer_cfg* cfg, double lambda_sel,
+                              double lambda_base, autoloco_outer_coeffs* out);
+
+/* ------------------------------------------------------------------------ */
+/* Adaptive interval controller (host)                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Settings of the controller and token mapper (Table "AutoLoCo
+ * configuration"; App. A).  Horizons h_* are token-equivalent horizons. */
+typedef struct {
+    int64_t h_base, h_min, h_max, q_h, budget_steps;
+    double beta_tok;      /* token-density EMA coefficient (0.9) */
+    double eps;           /* numerical constant of the residuals and the mapper */
+    double thr_cand, thr_mod, thr_sev; /* z_max class limits 1.5 / 2.5 / 4.0 */
+    double cand_exposure; /* candidate LR-exposure multiplier 1.15 */
+    double retire_frac;   /* rejected-bound retirement fraction 0.90 */
+    double red_moderate, red_severe; /* reduction divisors 1.20 / 1.50 */
+    double ref_ema;       /* log-space EMA coefficient of D_ref, C_ref */
+    double mad_scale, scale_floor; /* robust scale = max(mad_scale * MAD, scale_floor) */
+    int32_t n_mapper_boot, n_ref_boot, n_var, hist_max;   /* 3, 2, 3, 16 */
+    int32_t moderate_confirm, fallback_count;             /* 2, 2 */
+    autoloco_schedule sched;
+    autoloco_outer_cfg outer;
+} autoloco_controller_cfg;
+
+/* Fills *out with the C4 column of Table "AutoLoCo configuration" and the C4
+ * training recipe (50,000 steps, 1,000 warm-up steps, peak 4e-4, outer
+ * learning rate 0.7, momentum 0.9, no normalisation). */
+void autoloco_controller_default_cfg(autoloco_controller_cfg* out);
+
+/* What the trainer observed over the interval just completed. */
+typedef struct {
+    double D, C;          /* diagnostics of the round (autoloco_stats) */
+    double lambda_done;   /* learning-rate mass of the executed steps */
+    double tokens;        /* non-padding tokens processed (M_t) */
+    int64_t h_step_done;  /* executed local steps */
+    int32_t finite;       /* 0 if any required statistic was non-finite */
+} autoloco_observation;
+
+typedef enum {
+    AUTOLOCO_ASSESS_NONE = -1, AUTOLOCO_ASSESS_SUPPORTED = 0, AUTOLOCO_ASSESS_CONSISTENT = 1,
+    AUTOLOCO_ASSESS_MODERATE = 2, AUTOLOCO_ASSESS_SEVERE = 3, AUTOLOCO_ASSESS_INVALID = 4
+} autoloco_assessment;
+
+typedef enum {
+    AUTOLOCO_PHASE_WARMUP = 0, AUTOLOCO_PHASE_REF_BOOT = 1, AUTOLOCO_PHASE_INIT = 2,
+    AUTOLOCO_PHASE_VAR = 3, AUTOLOCO_PHASE_MONITOR = 4, AUTOLOCO_PHASE_CAND1 = 5,
+    AUTOLOCO_PHASE_CAND2 = 6, AUTOLOCO_PHASE_DONE = 7
+} autoloco_phase;
+
+/* The next interval: where it starts, its horizons, the previewed LR masses,
+ * the outer coefficients to use after it, and the assessment of the interval
+ * just observed. */
+typedef struct {
+    int64_t start_step, h_tok, h_step, h_ref;
+    double lambda_sel, lambda_base;
+    double z_max;          /* NaN when the observed interval was not assessed */
+    int32_t assessment;    /* autoloco_assessment of the observed interval */
+    int32_t phase;         /* autoloco_phase of the next interval */
+    int32_t done;          /* 1: the budget is spent, no next interval */
+    int32_t reserved;
+    autoloco_outer_coeffs coeffs;
+} autoloco_decision;
+
+/* The adaptive interval controller of Sec. "Adaptive Interval Selection" and
+ * App. A: residuals r_D, r_C against the accepted-horizon reference profile
+ * (eqs. adaptive-h-lr-mass, adaptive-h-core-residuals), robust deviation
+ * z_max (eq. adaptive-h-core-deviation), the assessment classes of Table
+ * "Interval assessments", candidate search and evaluation, rejected-horizon
+ * bound, reductions, and the token mapper (eq. adaptive-h-token-mapping).
+ * Not thread-safe; one controller per training run.
+ * create errors: E_INVALID (inconsistent settings), E_NOMEM. */
+typedef struct autoloco_controller autoloco_controller;
+int autoloco_controller_create(const autoloco_controller_cfg* cfg, autoloco_controller** out);
+void autoloco_controller_destroy(autoloco_controller* ctrl);
+
+/* First call: obs = NULL, returns the first interval.  Every later call:
+ * obs describes the interval returned by the previous call.  Once a decision
+ * with done = 1 has been returned, further calls fail with E_STATE.
+ * Errors: E_INVALID (null ctrl/next, missing or unexpected obs), E_STATE. */
+int autoloco_select_interval(autoloco_controller* ctrl, const autoloco_observation* obs,
+                             autoloco_decision* next);
+
+/* Current reference profile (D_ref, C_ref, Lambda_ref); zeros before it exists. */
+int autoloco_controller_reference(const autoloco_controller* ctrl, double* d_ref,
+                                  double* c_ref, double* lambda_ref);
+
+/* Checkpoint of the whole controller state.  save: with buf = NULL sets *len
+ * to the size needed; otherwise writes *len bytes (E_INVALID if *len is too
+ * small).  load: restores a state saved by the same library version into a
+ * controller created with any configuration (the saved configuration wins).
+ * Errors: E_INVALID (null pointers, bad size, bad magic or version). */
+int autoloco_controller_save(const autoloco_controller* ctrl, void* buf, size_t* len);
+int autoloco_controller_load(autoloco_controller* ctrl, const void* buf, size_t len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AUTOLOCO_H */

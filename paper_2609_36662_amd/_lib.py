@@ -1,0 +1,395 @@
+"""ctypes binding of libautoloco.so (the C ABI declared in include/autoloco.h).
+
+Argument marshalling only: torch tensors become raw device pointers and the
+context is bound to a HIP stream; every step of a round runs in the library.
+Loading fails loudly when the library is missing and cannot be built — there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+import threading
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+MAX_K = 16
+F32, BF16 = 0, 1
+FUSE_STATS, FUSE_RESET = 1, 2
+
+STATUS = {0: "ok", -1: "invalid argument", -2: "misaligned", -3: "aliasing buffers",
+          -4: "HIP runtime error", -5: "out of memory", -6: "call out of order"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libautoloco.so")
+
+
+class AutolocoError(RuntimeError):
+    def __init__(self, status: int, what: str, detail: str = ""):
+        self.status = status
+        msg = f"{what} failed: {STATUS.get(status, status)}"
+        if detail:
+            msg += f" ({detail})"
+        super().__init__(msg)
+
+
+# ------------------------------------------------------------------ structs --
+class Buffers(C.Structure):
+    _fields_ = [("n", C.c_int64), ("k", C.c_int32), ("replica_dtype", C.c_int32),
+                ("theta", C.c_void_p), ("momentum", C.c_void_p), ("replicas", C.c_void_p * MAX_K)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("sq_norm", C.c_double * MAX_K), ("sq_dev", C.c_double * MAX_K),
+                ("sq_mean", C.c_double), ("D", C.c_double), ("C", C.c_double),
+                ("disagreement", C.c_double), ("finite", C.c_int32), ("k", C.c_int32)]
+
+    def as_dict(self):
+        k = self.k
+        return {"sq_norm": list(self.sq_norm[:k]), "sq_dev": list(self.sq_dev[:k]),
+                "sq_mean": self.sq_mean, "D": self.D, "C": self.C,
+                "disagreement": self.disagreement, "finite": bool(self.finite)}
+
+
+class OuterCoeffs(C.Structure):
+    _fields_ = [("mu", C.c_double), ("eta_out", C.c_double), ("rho", C.c_double),
+                ("kappa", C.c_double), ("normalize", C.c_int32)]
+
+
+class Schedule(C.Structure):
+    _fields_ = [("peak", C.c_double), ("min_lr", C.c_double), ("warmup", C.c_int64),
+                ("total", C.c_int64)]
+
+
+class OuterCfg(C.Structure):
+    _fields_ = [("eta_base", C.c_double), ("mu_base", C.c_double), ("mu_min", C.c_double),
+                ("mu_max", C.c_double), ("kappa_max", C.c_double), ("eps", C.c_double),
+                ("normalize", C.c_int32)]
+
+
+class ControllerCfg(C.Structure):
+    _fields_ = [("h_base", C.c_int64), ("h_min", C.c_int64), ("h_max", C.c_int64),
+                ("q_h", C.c_int64), ("budget_steps", C.c_int64),
+                ("beta_tok", C.c_double), ("eps", C.c_double), ("thr_cand", C.c_double),
+                ("thr_mod", C.c_double), ("thr_sev", C.c_double), ("cand_exposure", C.c_double),
+                ("retire_frac", C.c_double), ("red_moderate", C.c_double),
+                ("red_severe", C.c_double), ("ref_ema", C.c_double), ("mad_scale", C.c_double),
+                ("scale_floor", C.c_double),
+                ("n_mapper_boot", C.c_int32), ("n_ref_boot", C.c_int32), ("n_var", C.c_int32),
+                ("hist_max", C.c_int32), ("moderate_confirm", C.c_int32),
+                ("fallback_count", C.c_int32),
+                ("sched", Schedule), ("outer", OuterCfg)]
+
+
+class Observation(C.Structure):
+    _fields_ = [("D", C.c_double), ("C", C.c_double), ("lambda_done", C.c_double),
+                ("tokens", C.c_double), ("h_step_done", C.c_int64), ("finite", C.c_int32)]
+
+
+class Decision(C.Structure):
+    _fields_ = [("start_step", C.c_int64), ("h_tok", C.c_int64), ("h_step", C.c_int64),
+                ("h_ref", C.c_int64), ("lambda_sel", C.c_double), ("lambda_base", C.c_double),
+                ("z_max", C.c_double), ("assessment", C.c_int32), ("phase", C.c_int32),
+                ("done", C.c_int32), ("reserved", C.c_int32), ("coeffs", OuterCoeffs)]
+
+
+# ---------------------------------------------------------------- loading --
+_lib = None
+_lock = threading.Lock()
+
+# (name, restype, argtypes) of every symbol the header declares
+SYMBOLS = [
+    ("autoloco_status_string", C.c_char_p, [C.c_int]),
+    ("autoloco_create", C.c_int, [C.c_int, C.c_void_p, C.POINTER(C.c_void_p)]),
+    ("autoloco_destroy", None, [C.c_void_p]),
+    ("autoloco_last_error", C.c_char_p, [C.c_void_p]),
+    ("autoloco_set_timing", C.c_int, [C.c_void_p, C.c_int]),
+    ("autoloco_last_kernel_ms", C.c_int, [C.c_void_p, C.POINTER(C.c_float)]),
+    ("autoloco_set_grid_limit", C.c_int, [C.c_void_p, C.c_int]),
+    ("autoloco_launch_shape", C.c_int, [C.c_void_p, C.c_int64, C.c_int32, C.POINTER(C.c_int32),
+                                        C.POINTER(C.c_int32)]),
+    ("autoloco_round_stats", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.c_double, C.POINTER(Stats)]),
+    ("autoloco_outer_step", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
+                                      C.c_uint32, C.c_double, C.POINTER(Stats)]),
+    ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
+    ("autoloco_inner_lr", C.c_double, [C.POINTER(Schedule), C.c_int64]),
+    ("autoloco_lr_mass", C.c_double, [C.POINTER(Schedule), C.c_int64, C.c_int64]),
+    ("autoloco_outer_correction", C.c_int, [C.POINTER(OuterCfg), C.c_double, C.c_double,
+                                            C.POINTER(OuterCoeffs)]),
+    ("autoloco_controller_default_cfg", None, [C.POINTER(ControllerCfg)]),
+    ("autoloco_controller_create", C.c_int, [C.POINTER(ControllerCfg), C.POINTER(C.c_void_p)]),
+    ("autoloco_controller_destroy", None, [C.c_void_p]),
+    ("autoloco_select_interval", C.c_int, [C.c_void_p, C.POINTER(Observation), C.POINTER(Decision)]),
+    ("autoloco_controller_reference", C.c_int, [C.c_void_p, C.POINTER(C.c_double),
+                                                C.POINTER(C.c_double), C.POINTER(C.c_double)]),
+    ("autoloco_controller_save", C.c_int, [C.c_void_p, C.c_void_p, C.POINTER(C.c_size_t)]),
+    ("autoloco_controller_load", C.c_int, [C.c_void_p, C.c_void_p, C.c_size_t]),
+]
+
+
+def lib():
+    """The loaded library; builds it first if nothing is built yet."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                from . import build as _build
+                _build.build()
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing and could not be built")
+            handle = C.CDLL(LIB_PATH)
+            for name, res, args in SYMBOLS:
+                fn = getattr(handle, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = handle
+        return _lib
+
+
+def _check(status: int, what: str, ctx: Optional["Context"] = None):
+    if status != 0:
+        detail = ""
+        if ctx is not None and ctx.handle:
+            detail = lib().autoloco_last_error(ctx.handle).decode()
+        raise AutolocoError(status, what, detail)
+
+
+# ----------------------------------------------------------------- context --
+class Context:
+    """An autoloco_ctx bound to one device and one HIP stream."""
+
+    def __init__(self, device: int = 0, stream=None):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("the AutoLoCo round library needs a GPU; none is visible")
+        if stream is None:
+            stream = torch.cuda.current_stream(device)
+        self.stream = stream
+        raw = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        h = C.c_void_p()
+        _check(lib().autoloco_create(device, C.c_void_p(raw), C.byref(h)), "autoloco_create")
+        self.handle = h
+        self.device = device
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().autoloco_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def autoloco_create(device: int = 0, stream=None) -> Context:
+    return Context(device, stream)
+
+
+def autoloco_destroy(ctx: Context) -> None:
+    ctx.close()
+
+
+def autoloco_last_error(ctx: Context) -> str:
+    return lib().autoloco_last_error(ctx.handle).decode()
+
+
+def autoloco_set_timing(ctx: Context, enable: bool) -> None:
+    _check(lib().autoloco_set_timing(ctx.handle, int(bool(enable))), "autoloco_set_timing", ctx)
+
+
+def autoloco_last_kernel_ms(ctx: Context) -> float:
+    ms = C.c_float()
+    _check(lib().autoloco_last_kernel_ms(ctx.handle, C.byref(ms)), "autoloco_last_kernel_ms", ctx)
+    return ms.value
+
+
+def autoloco_set_grid_limit(ctx: Context, max_blocks: int) -> None:
+    _check(lib().autoloco_set_grid_limit(ctx.handle, int(max_blocks)), "autoloco_set_grid_limit", ctx)
+
+
+def autoloco_launch_shape(ctx: Context, n: int, replica_dtype: int = F32):
+    b, t = C.c_int32(), C.c_int32()
+    _check(lib().autoloco_launch_shape(ctx.handle, int(n), int(replica_dtype), C.byref(b), C.byref(t)),
+           "autoloco_launch_shape", ctx)
+    return b.value, t.value
+
+
+# ----------------------------------------------------------- marshalling --
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"replicas must be float32 or bfloat16, got {t.dtype}")
+
+
+def make_buffers(theta, replicas: Sequence, momentum=None, n: Optional[int] = None) -> Buffers:
+    """Describe caller-owned device tensors to the library (no copies)."""
+    import torch
+    reps = list(replicas)
+    if not 1 <= len(reps) <= MAX_K:
+        raise ValueError(f"need 1..{MAX_K} replicas, got {len(reps)}")
+    ts = [theta] + reps + ([momentum] if momentum is not None else [])
+    for t in ts:
+        if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+            raise TypeError("all buffers must be CUDA (HIP) tensors")
+        if not t.is_contiguous():
+            raise ValueError("all buffers must be contiguous")
+    if theta.dtype != torch.float32 or (momentum is not None and momentum.dtype != torch.float32):
+        raise TypeError("theta and momentum must be float32")
+    code = _dtype_code(reps[0])
+    if any(_dtype_code(r) != code for r in reps):
+        raise TypeError("all replicas must share one dtype")
+    count = theta.numel() if n is None else int(n)
+    if any(t.numel() < count for t in ts):
+        raise ValueError("a buffer is shorter than n")
+    b = Buffers()
+    b.n = count
+    b.k = len(reps)
+    b.replica_dtype = code
+    b.theta = theta.data_ptr()
+    b.momentum = momentum.data_ptr() if momentum is not None else None
+    for i, r in enumerate(reps):
+        b.replicas[i] = r.data_ptr()
+    return b
+
+
+def make_coeffs(mu: float, eta_out: float, rho: float = 1.0, normalize: bool = False,
+                kappa: float = float("nan")) -> OuterCoeffs:
+    c = OuterCoeffs()
+    c.mu, c.eta_out, c.rho, c.kappa, c.normalize = mu, eta_out, rho, kappa, int(bool(normalize))
+    return c
+
+
+def autoloco_round_stats(ctx: Context, theta, replicas, eps: float = 1e-12, n=None) -> Stats:
+    b = make_buffers(theta, replicas, None, n)
+    out = Stats()
+    _check(lib().autoloco_round_stats(ctx.handle, C.byref(b), eps, C.byref(out)), "autoloco_round_stats", ctx)
+    return out
+
+
+def autoloco_outer_step(ctx: Context, theta, momentum, replicas, coeffs: OuterCoeffs,
+                        flags: int = FUSE_STATS | FUSE_RESET, eps: float = 1e-12, n=None) -> Optional[Stats]:
+    b = make_buffers(theta, replicas, momentum, n)
+    out = Stats()
+    _check(lib().autoloco_outer_step(ctx.handle, C.byref(b), C.byref(coeffs), flags, eps,
+                                     C.byref(out) if flags & FUSE_STATS else None),
+           "autoloco_outer_step", ctx)
+    return out if flags & FUSE_STATS else None
+
+
+def autoloco_broadcast_reset(ctx: Context, theta, replicas, n=None) -> None:
+    b = make_buffers(theta, replicas, None, n)
+    _check(lib().autoloco_broadcast_reset(ctx.handle, C.byref(b)), "autoloco_broadcast_reset", ctx)
+
+
+# -------------------------------------------------------- host scalars --
+def make_schedule(peak=4e-4, min_lr=0.0, warmup=1000, total=50_000) -> Schedule:
+    s = Schedule()
+    s.peak, s.min_lr, s.warmup, s.total = peak, min_lr, warmup, total
+    return s
+
+
+def autoloco_inner_lr(sched: Schedule, step: int) -> float:
+    return lib().autoloco_inner_lr(C.byref(sched), step)
+
+
+def autoloco_lr_mass(sched: Schedule, start_step: int, steps: int) -> float:
+    return lib().autoloco_lr_mass(C.byref(sched), start_step, steps)
+
+
+def make_outer_cfg(eta_base=0.7, mu_base=0.9, mu_min=0.45, mu_max=0.90, kappa_max=1.6,
+                   eps=1e-12, normalize=False) -> OuterCfg:
+    c = OuterCfg()
+    c.eta_base, c.mu_base, c.mu_min, c.mu_max = eta_base, mu_base, mu_min, mu_max
+    c.kappa_max, c.eps, c.normalize = kappa_max, eps, int(bool(normalize))
+    return c
+
+
+def autoloco_outer_correction(cfg: OuterCfg, lambda_sel: float, lambda_base: float) -> OuterCoeffs:
+    out = OuterCoeffs()
+    _check(lib().autoloco_outer_correction(C.byref(cfg), lambda_sel, lambda_base, C.byref(out)),
+           "autoloco_outer_correction")
+    return out
+
+
+def default_controller_cfg(**overrides) -> ControllerCfg:
+    c = ControllerCfg()
+    lib().autoloco_controller_default_cfg(C.byref(c))
+    for key, val in overrides.items():
+        if key == "sched":
+            c.sched = val
+        elif key == "outer":
+            c.outer = val
+        else:
+            setattr(c, key, val)
+    return c
+
+
+class Controller:
+    """An autoloco_controller."""
+
+    def __init__(self, cfg: Optional[ControllerCfg] = None):
+        cfg = cfg if cfg is not None else default_controller_cfg()
+        h = C.c_void_p()
+        _check(lib().autoloco_controller_create(C.byref(cfg), C.byref(h)), "autoloco_controller_create")
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().autoloco_controller_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def autoloco_controller_create(cfg: Optional[ControllerCfg] = None) -> Controller:
+    return Controller(cfg)
+
+
+def make_observation(D, C_, lambda_done, tokens, h_step_done, finite=True) -> Observation:
+    o = Observation()
+    o.D, o.C, o.lambda_done, o.tokens = D, C_, lambda_done, tokens
+    o.h_step_done, o.finite = int(h_step_done), int(bool(finite))
+    return o
+
+
+def autoloco_select_interval(ctrl: Controller, obs: Optional[Observation]) -> Decision:
+    out = Decision()
+    _check(lib().autoloco_select_interval(ctrl.handle, C.byref(obs) if obs is not None else None,
+                                          C.byref(out)), "autoloco_select_interval")
+    return out
+
+
+def autoloco_controller_reference(ctrl: Controller):
+    d, c, l = C.c_double(), C.c_double(), C.c_double()
+    _check(lib().autoloco_controller_reference(ctrl.handle, C.byref(d), C.byref(c), C.byref(l)),
+           "autoloco_controller_reference")
+    return d.value, c.value, l.value
+
+
+def autoloco_controller_save(ctrl: Controller) -> bytes:
+    n = C.c_size_t(0)
+    _check(lib().autoloco_controller_save(ctrl.handle, None, C.byref(n)), "autoloco_controller_save")
+    buf = C.create_string_buffer(n.value)
+    _check(lib().autoloco_controller_save(ctrl.handle, buf, C.byref(n)), "autoloco_controller_save")
+    return buf.raw[: n.value]
+
+
+def autoloco_controller_load(ctrl: Controller, blob: bytes) -> None:
+    buf = C.create_string_buffer(blob, len(blob))
+    _check(lib().autoloco_controller_load(ctrl.handle, buf, len(blob)), "autoloco_controller_load")

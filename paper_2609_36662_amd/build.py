@@ -1,0 +1,81 @@
+"""Build the AutoLoCo round library (libautoloco.so) in-tree for gfx950.
+
+The round kernels are compiled as ten slices (replica type x mode) in
+parallel; the host-side scalar code (schedule, correction, controller) is
+plain C++ built with g++ without floating-point contraction; hipcc links the
+shared library next to this file.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(PKG, "_build")
+LIB = os.path.join(PKG, "libautoloco.so")
+ARCH = "gfx950"
+
+HIP_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+    # no packed-fp32 instructions anywhere in the device code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    f"-I{INCLUDE}", f"-I{CSRC}",
+]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-fno-fast-math", f"-I{INCLUDE}"]
+
+
+def _hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found: the ROCm toolchain is required to build libautoloco.so")
+
+
+def _run(cmd):
+    proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    out = "\n".join(l for l in proc.stdout.splitlines() if "packed-fp32-ops" not in l
+                    and "target feature" not in l)
+    if proc.returncode != 0:
+        raise RuntimeError(f"build step failed ({proc.returncode}): {' '.join(cmd)}\n{out}")
+    return out
+
+
+def jobs():
+    hipcc = _hipcc()
+    cmds = []
+    for rt, rtname in ((0, "f32"), (1, "bf16")):
+        for mode in range(5):
+            obj = os.path.join(BUILD, f"round_{rtname}_m{mode}.o")
+            cmds.append([hipcc, *HIP_FLAGS, f"-DAL_RT={rt}", f"-DAL_RTNAME={rtname}", f"-DAL_MODE={mode}",
+                         "-c", os.path.join(CSRC, "round_inst.hip"), "-o", obj])
+    cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "api.hip"), "-o", os.path.join(BUILD, "api.o")])
+    for src in ("scalar.cpp", "controller.cpp"):
+        cmds.append(["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, src),
+                     "-o", os.path.join(BUILD, src.replace(".cpp", ".o"))])
+    return hipcc, cmds
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link libautoloco.so; returns its path."""
+    os.makedirs(BUILD, exist_ok=True)
+    hipcc, cmds = jobs()
+    workers = max(1, min(len(cmds), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(workers) as pool:
+        for out in pool.map(_run, cmds):
+            if verbose and out.strip():
+                print(out)
+    objs = [c[c.index("-o") + 1] for c in cmds]
+    tmp = LIB + ".tmp"
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

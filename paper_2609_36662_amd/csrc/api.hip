@@ -1,0 +1,377 @@
+// Device entry points of the C ABI: context, argument validation, launch
+// shape and dispatch to the round kernels.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "autoloco.h"
+#include "round_kernels.hpp"
+
+using namespace autoloco;
+
+namespace {
+
+constexpr int kBlocksPerCu = 8;     // default grid: 8 workgroups of 256 per compute unit
+constexpr int kMaxBlocks = 16384;   // scratch sized for this many workgroups
+
+}  // namespace
+
+struct autoloco_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int num_cus = 0;
+    int grid_limit = 0;
+    double* partials = nullptr;
+    unsigned int* ticket = nullptr;
+    double* sums = nullptr;
+    double* host_sums = nullptr;
+    bool timing = false;
+    bool timed_valid = false;
+    hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+    std::string err;
+};
+
+namespace {
+
+// Makes the context's device current for the duration of a call.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+int fail(autoloco_ctx* ctx, int code, const std::string& msg) {
+    if (ctx) ctx->err = msg;
+    return code;
+}
+
+int hip_fail(autoloco_ctx* ctx, hipError_t e, const char* what) {
+    return fail(ctx, AUTOLOCO_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t replica_size(int32_t dtype) { return dtype == AUTOLOCO_BF16 ? 2 : 4; }
+
+int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype) {
+    const int64_t v = dtype == AUTOLOCO_BF16 ? 8 : 4;
+    const int64_t nvec = n / v;
+    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * kBlocksPerCu;
+    if (limit > kMaxBlocks) limit = kMaxBlocks;
+    int64_t want = (nvec + kBlock - 1) / kBlock;
+    if (want < 1) want = 1;
+    return static_cast<int>(want < limit ? want : limit);
+}
+
+struct Range {
+    uintptr_t lo, hi;
+    const char* name;
+};
+
+// Checks pointers, sizes, alignment and overlap.  need_momentum: the call
+// reads and writes the momentum buffer.
+int validate(autoloco_ctx* ctx, const autoloco_buffers* b, bool need_momentum) {
+    if (ctx == nullptr) return AUTOLOCO_E_INVALID;
+    if (b == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null buffers");
+    if (b->n < 0) return fail(ctx, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(ctx, AUTOLOCO_E_INVALID, "k outside 1..16");
+    if (b->replica_dtype != AUTOLOCO_F32 && b->replica_dtype != AUTOLOCO_BF16)
+        return fail(ctx, AUTOLOCO_E_INVALID, "unknown replica dtype");
+    if (b->n == 0) return AUTOLOCO_OK;
+    Range r[AUTOLOCO_MAX_K + 2];
+    int nr = 0;
+    const uintptr_t fbytes = static_cast<uintptr_t>(b->n) * 4u;
+    const uintptr_t rbytes = static_cast<uintptr_t>(b->n) * replica_size(b->replica_dtype);
+    if (b->theta == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null theta");
+    r[nr++] = {reinterpret_cast<uintptr_t>(b->theta), reinterpret_cast<uintptr_t>(b->theta) + fbytes, "theta"};
+    if (need_momentum) {
+        if (b->momentum == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null momentum");
+        r[nr++] = {reinterpret_cast<uintptr_t>(b->momentum), reinterpret_cast<uintptr_t>(b->momentum) + fbytes,
+                   "momentum"};
+    }
+    for (int k = 0; k < b->k; ++k) {
+        if (b->replicas[k] == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null replica " + std::to_string(k));
+        const uintptr_t p = reinterpret_cast<uintptr_t>(b->replicas[k]);
+        r[nr++] = {p, p + rbytes, "replica"};
+    }
+    for (int i = 0; i < nr; ++i)
+        if (r[i].lo % 16 != 0) return fail(ctx, AUTOLOCO_E_ALIGN, std::string(r[i].name) + " not 16-byte aligned");
+    for (int i = 0; i < nr; ++i)
+        for (int j = i + 1; j < nr; ++j)
+            if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
+                return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    return AUTOLOCO_OK;
+}
+
+void finish_stats(const double* sums, int k, double eps, autoloco_stats* out) {
+    std::memset(out, 0, sizeof(*out));
+    out->k = k;
+    double ts = 0.0, tq = 0.0;
+    for (int i = 0; i < k; ++i) {
+        out->sq_norm[i] = sums[i];
+        out->sq_dev[i] = sums[k + i];
+        ts += sums[i];
+        tq += sums[k + i];
+    }
+    out->sq_mean = sums[2 * k];
+    out->D = ts / k;
+    out->C = k * out->sq_mean / (out->D + eps);
+    out->disagreement = tq / k;
+    bool fin = std::isfinite(out->sq_mean) && std::isfinite(out->D) && std::isfinite(out->C) &&
+               std::isfinite(out->disagreement);
+    for (int i = 0; i < k; ++i) fin = fin && std::isfinite(out->sq_norm[i]) && std::isfinite(out->sq_dev[i]);
+    out->finite = fin ? 1 : 0;
+}
+
+RoundLauncher launcher(int32_t dtype, int mode) {
+    static const RoundLauncher f32[MODE_COUNT] = {launch_round_f32_m0, launch_round_f32_m1, launch_round_f32_m2,
+                                                  launch_round_f32_m3, launch_round_f32_m4};
+    static const RoundLauncher bf16[MODE_COUNT] = {launch_round_bf16_m0, launch_round_bf16_m1,
+                                                   launch_round_bf16_m2, launch_round_bf16_m3,
+                                                   launch_round_bf16_m4};
+    return dtype == AUTOLOCO_BF16 ? bf16[mode] : f32[mode];
+}
+
+RoundArgs make_args(autoloco_ctx* ctx, const autoloco_buffers* b) {
+    RoundArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.theta = b->theta;
+    a.momentum = b->momentum;
+    for (int k = 0; k < b->k; ++k) a.replicas[k] = b->replicas[k];
+    a.n = b->n;
+    a.mu = 0.f;
+    a.eta = 0.f;
+    a.scale = 1.f;
+    a.inv_k = 1.0f / static_cast<float>(b->k);
+    a.partials = ctx->partials;
+    a.ticket = ctx->ticket;
+    a.sums = ctx->sums;
+    return a;
+}
+
+// Launches one round kernel (timed if requested); with stats, waits for the
+// sums and fills *out.
+int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, int mode, bool stats,
+              double eps, autoloco_stats* out) {
+    const int blocks = blocks_for(ctx, b->n, b->replica_dtype);
+    hipError_t e;
+    if (ctx->timing && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    e = launcher(b->replica_dtype, mode)(b->k, blocks, ctx->stream, a);
+    if (e != hipSuccess) return hip_fail(ctx, e, "kernel launch");
+    if (ctx->timing) {
+        if ((e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+        ctx->timed_valid = true;
+    }
+    if (stats) {
+        const size_t bytes = sizeof(double) * (2 * b->k + 1);
+        e = hipMemcpyAsync(ctx->host_sums, ctx->sums, bytes, hipMemcpyDeviceToHost, ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipMemcpyAsync");
+        e = hipStreamSynchronize(ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+        finish_stats(ctx->host_sums, b->k, eps, out);
+    }
+    ctx->err.clear();
+    return AUTOLOCO_OK;
+}
+
+void zero_stats(int k, double eps, autoloco_stats* out) {
+    double z[kMaxSums] = {0};
+    finish_stats(z, k, eps, out);
+}
+
+}  // namespace
+
+extern "C" {
+
+int autoloco_create(int device, void* stream, autoloco_ctx** out) {
+    if (out == nullptr) return AUTOLOCO_E_INVALID;
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count) return AUTOLOCO_E_INVALID;
+    DeviceGuard g(device);
+    if (!g.ok) return AUTOLOCO_E_DEVICE;
+    auto* c = new (std::nothrow) autoloco_ctx;
+    if (c == nullptr) return AUTOLOCO_E_NOMEM;
+    c->device = device;
+    c->stream = static_cast<hipStream_t>(stream);
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) != hipSuccess) {
+        delete c;
+        return AUTOLOCO_E_DEVICE;
+    }
+    c->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+    bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
+              hipMalloc(&c->ticket, 256) == hipSuccess &&
+              hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
+              hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocDefault) == hipSuccess;
+    ok = ok && hipMemset(c->ticket, 0, 256) == hipSuccess && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
+    ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess;
+    ok = ok && hipDeviceSynchronize() == hipSuccess;
+    if (!ok) {
+        autoloco_destroy(c);
+        return AUTOLOCO_E_NOMEM;
+    }
+    *out = c;
+    return AUTOLOCO_OK;
+}
+
+void autoloco_destroy(autoloco_ctx* c) {
+    if (c == nullptr) return;
+    {
+        DeviceGuard g(c->device);
+        (void)hipStreamSynchronize(c->stream);
+        if (c->partials) (void)hipFree(c->partials);
+        if (c->ticket) (void)hipFree(c->ticket);
+        if (c->sums) (void)hipFree(c->sums);
+        if (c->host_sums) (void)hipHostFree(c->host_sums);
+        if (c->ev_start) (void)hipEventDestroy(c->ev_start);
+        if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
+    }
+    delete c;
+}
+
+const char* autoloco_last_error(const autoloco_ctx* c) { return c == nullptr ? "null context" : c->err.c_str(); }
+
+int autoloco_set_timing(autoloco_ctx* c, int enable) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    c->timing = enable != 0;
+    c->timed_valid = false;
+    return AUTOLOCO_OK;
+}
+
+int autoloco_last_kernel_ms(autoloco_ctx* c, float* ms) {
+    if (c == nullptr || ms == nullptr) return AUTOLOCO_E_INVALID;
+    if (!c->timed_valid) return fail(c, AUTOLOCO_E_STATE, "no timed launch yet");
+    DeviceGuard g(c->device);
+    hipError_t e = hipEventSynchronize(c->ev_stop);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
+    e = hipEventElapsedTime(ms, c->ev_start, c->ev_stop);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
+    return AUTOLOCO_OK;
+}
+
+int autoloco_set_grid_limit(autoloco_ctx* c, int max_blocks) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (max_blocks < 0 || max_blocks > kMaxBlocks)
+        return fail(c, AUTOLOCO_E_INVALID, "grid limit outside 0..16384");
+    c->grid_limit = max_blocks;
+    return AUTOLOCO_OK;
+}
+
+int autoloco_launch_shape(const autoloco_ctx* c, int64_t n, int32_t dtype, int32_t* blocks, int32_t* threads) {
+    if (c == nullptr || blocks == nullptr || threads == nullptr || n < 0) return AUTOLOCO_E_INVALID;
+    if (dtype != AUTOLOCO_F32 && dtype != AUTOLOCO_BF16) return AUTOLOCO_E_INVALID;
+    *blocks = blocks_for(c, n, dtype);
+    *threads = kBlock;
+    return AUTOLOCO_OK;
+}
+
+int autoloco_round_stats(autoloco_ctx* c, const autoloco_buffers* b, double eps, autoloco_stats* out) {
+    int st = validate(c, b, false);
+    if (st != AUTOLOCO_OK) return st;
+    if (out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null stats output");
+    if (!(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    if (b->n == 0) {
+        zero_stats(b->k, eps, out);
+        return AUTOLOCO_OK;
+    }
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RoundArgs a = make_args(c, b);
+    return run_round(c, b, a, MODE_STATS, true, eps, out);
+}
+
+int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
+                        uint32_t flags, double eps, autoloco_stats* out) {
+    int st = validate(c, b, true);
+    if (st != AUTOLOCO_OK) return st;
+    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
+    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
+    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
+    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
+    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
+    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
+        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    if (b->n == 0) {
+        if (stats) zero_stats(b->k, eps, out);
+        return AUTOLOCO_OK;
+    }
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RoundArgs a = make_args(c, b);
+    a.mu = static_cast<float>(co->mu);
+    a.eta = static_cast<float>(co->eta_out);
+    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    const int mode = stats ? (reset ? MODE_UPDATE_STATS_RESET : MODE_UPDATE_STATS)
+                           : (reset ? MODE_UPDATE_RESET : MODE_UPDATE);
+    return run_round(c, b, a, mode, stats, eps, out);
+}
+
+int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
+    int st = validate(c, b, false);
+    if (st != AUTOLOCO_OK) return st;
+    if (b->n == 0) return AUTOLOCO_OK;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RoundArgs a = make_args(c, b);
+    const int blocks = blocks_for(c, b->n, b->replica_dtype);
+    hipError_t e;
+    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if (c->timing) {
+        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+        c->timed_valid = true;
+    }
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------ reset launcher
+namespace autoloco {
+namespace {
+template <int K>
+hipError_t reset_k(int rt, int blocks, hipStream_t s, const RoundArgs& a) {
+    if (rt == RT_BF16)
+        hipLaunchKernelGGL((reset_kernel<K, RT_BF16>), dim3(blocks), dim3(kBlock), 0, s, a);
+    else
+        hipLaunchKernelGGL((reset_kernel<K, RT_F32>), dim3(blocks), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_reset(int rt, int k, int blocks, hipStream_t s, const RoundArgs& a) {
+    switch (k) {
+        case 1: return reset_k<1>(rt, blocks, s, a);
+        case 2: return reset_k<2>(rt, blocks, s, a);
+        case 3: return reset_k<3>(rt, blocks, s, a);
+        case 4: return reset_k<4>(rt, blocks, s, a);
+        case 5: return reset_k<5>(rt, blocks, s, a);
+        case 6: return reset_k<6>(rt, blocks, s, a);
+        case 7: return reset_k<7>(rt, blocks, s, a);
+        case 8: return reset_k<8>(rt, blocks, s, a);
+        case 9: return reset_k<9>(rt, blocks, s, a);
+        case 10: return reset_k<10>(rt, blocks, s, a);
+        case 11: return reset_k<11>(rt, blocks, s, a);
+        case 12: return reset_k<12>(rt, blocks, s, a);
+        case 13: return reset_k<13>(rt, blocks, s, a);
+        case 14: return reset_k<14>(rt, blocks, s, a);
+        case 15: return reset_k<15>(rt, blocks, s, a);
+        case 16: return reset_k<16>(rt, blocks, s, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+}  // namespace autoloco

@@ -1,0 +1,384 @@
+// Streaming kernels of one AutoLoCo synchronisation round on gfx950.
+//
+// One pass over the parameters reads theta_t, v_{t-1} and the K worker
+// replicas once, and (depending on the mode) writes theta_{t+1}, v_t and the
+// K reset replicas once.  Per parameter j:
+//   Delta_k   = theta[j] - theta_k[j]                  (Alg. "AutoLoCo outer interval")
+//   Delta_bar = (sum_k Delta_k) * (1/K)                pairwise tree over k in index order
+//   S_k += Delta_k^2, Q_k += (Delta_k - Delta_bar)^2, M += Delta_bar^2
+//                                                      (eq. adaptive-h-core-diagnostics; App. C.1)
+//   Dt = Delta_bar * scale   (scale = 1/rho when normalising, else 1; eq. normalized-pseudo-gradient)
+//   v' = mu v + Dt; d = Dt + mu v'; theta' = theta - eta d   (eq. autoloco-corrected-nesterov)
+//   theta_k[j] = theta'  (fp32, or bf16 rounded to nearest even)
+//
+// Nothing here is a contraction, so no matrix cores are used: the work is
+// bound by HBM bandwidth.  Each lane moves 16-byte vectors (4 fp32 or 8 bf16
+// parameters) with non-temporal loads and stores so the streams do not
+// displace one another in the caches, in a grid-stride loop over a fixed
+// grid.  Elementwise arithmetic is fp32; the squared sums of one vector are
+// added in fp32 and then into per-lane fp64 running sums.  The 2K+1 sums are
+// reduced deterministically: a wavefront butterfly, then the waves of the
+// workgroup in order through LDS into one partial per workgroup, then the
+// last workgroup to finish (found with an atomic counter) adds the partials
+// in workgroup order.  With the grid fixed, every run adds the same numbers
+// in the same order, so the statistics are bit-identical between runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace autoloco {
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxK = 16;
+constexpr int kMaxSums = 2 * kMaxK + 1;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+enum ReplicaType { RT_F32 = 0, RT_BF16 = 1 };
+enum Mode { MODE_STATS = 0, MODE_UPDATE = 1, MODE_UPDATE_STATS = 2, MODE_UPDATE_RESET = 3,
+            MODE_UPDATE_STATS_RESET = 4, MODE_COUNT = 5 };
+
+struct RoundArgs {
+    float* theta;
+    float* momentum;
+    void* replicas[kMaxK];
+    int64_t n;
+    float mu, eta, scale, inv_k;
+    double* partials;      // [gridDim.x][2K+1]
+    unsigned int* ticket;  // zero between launches
+    double* sums;          // [2K+1] final sums
+};
+
+// ------------------------------------------------------------------ memory --
+__device__ __forceinline__ f32x4 ld_f4(const float* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+}
+__device__ __forceinline__ void st_f4(float* p, f32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+}
+__device__ __forceinline__ u32x4 ld_u4(const void* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void st_u4(void* p, u32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+// bf16 <-> fp32.  Widening is exact; narrowing rounds to nearest, ties to
+// even, keeps infinities and turns every NaN into the quiet NaN 0x7FC0 with
+// its sign.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) & 0x8000u) | 0x7fc0u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
+    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
+// ------------------------------------------------------------- arithmetic --
+template <int LO, int CNT, int K>
+__device__ __forceinline__ float tree_sum(const float (&d)[K]) {
+    if constexpr (CNT == 1) {
+        return d[LO];
+    } else {
+        constexpr int H = CNT / 2;
+        return tree_sum<LO, H, K>(d) + tree_sum<LO + H, CNT - H, K>(d);
+    }
+}
+
+// One parameter: pseudo-gradients, their mean, the squared-sum terms and the
+// corrected Nesterov step.
+template <int K, bool STATS, bool UPDATE>
+__device__ __forceinline__ void one_param(float th, float v, const float (&r)[K], const RoundArgs& a,
+                                          float (&s)[K], float (&q)[K], float& m, float& th_new,
+                                          float& v_new) {
+    float d[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) d[k] = th - r[k];
+    const float mean = tree_sum<0, K, K>(d) * a.inv_k;
+    if constexpr (STATS) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            s[k] = __builtin_fmaf(d[k], d[k], s[k]);
+            const float e = d[k] - mean;
+            q[k] = __builtin_fmaf(e, e, q[k]);
+        }
+        m = __builtin_fmaf(mean, mean, m);
+    }
+    if constexpr (UPDATE) {
+        const float dt = mean * a.scale;
+        v_new = __builtin_fmaf(a.mu, v, dt);
+        const float dir = __builtin_fmaf(a.mu, v_new, dt);
+        th_new = __builtin_fmaf(-a.eta, dir, th);
+    }
+}
+
+// --------------------------------------------------------------- reduction --
+// Sums acc[0..NS) over the workgroup; the result is valid in threads
+// 0..NS-1 (thread j holds sum j).  Fixed order throughout.
+template <int NS>
+__device__ __forceinline__ double block_reduce(double (&acc)[NS], double* lds) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        double v = acc[j];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        acc[j] = v;
+    }
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < NS; ++j) lds[wave * NS + j] = acc[j];
+    }
+    __syncthreads();
+    double t = 0.0;
+    if (threadIdx.x < NS) {
+        t = lds[threadIdx.x];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) t += lds[w * NS + threadIdx.x];
+    }
+    __syncthreads();
+    return t;
+}
+
+// Stage 1 writes this workgroup's partials; the last workgroup to arrive
+// adds all partials in workgroup order and writes the final sums.
+template <int NS>
+__device__ __forceinline__ void grid_reduce(double (&acc)[NS], const RoundArgs& a) {
+    __shared__ double lds[kWaves * kMaxSums];
+    __shared__ int is_last;
+    const double part = block_reduce<NS>(acc, lds);
+    if (threadIdx.x < NS)
+        __hip_atomic_store(&a.partials[(int64_t)blockIdx.x * NS + threadIdx.x], part, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned int prev =
+            __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        is_last = (prev == gridDim.x - 1);
+    }
+    __syncthreads();
+    if (!is_last) return;
+    __threadfence();
+    double tot[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) tot[j] = 0.0;
+    for (unsigned int b = threadIdx.x; b < gridDim.x; b += kBlock) {
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+            tot[j] += __hip_atomic_load(&a.partials[(int64_t)b * NS + j], __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const double fin = block_reduce<NS>(tot, lds);
+    if (threadIdx.x < NS) a.sums[threadIdx.x] = fin;
+    if (threadIdx.x == 0) __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------ round kernel --
+template <int K, int RT, bool STATS, bool UPDATE, bool RESET>
+__global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
+    constexpr int V = RT == RT_F32 ? 4 : 8;  // parameters per 16-byte replica vector
+    constexpr int NS = STATS ? 2 * K + 1 : 1;
+    double acc[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) acc[j] = 0.0;
+
+    const int64_t nvec = a.n / V;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+
+    for (int64_t i = gtid; i < nvec; i += stride) {
+        const int64_t base = i * V;
+        float th[V], v[V], r[K][V];
+        if constexpr (RT == RT_F32) {
+            const f32x4 t4 = ld_f4(a.theta + base);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) th[e] = t4[e];
+            if constexpr (UPDATE) {
+                const f32x4 v4 = ld_f4(a.momentum + base);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = v4[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const f32x4 r4 = ld_f4(static_cast<const float*>(a.replicas[k]) + base);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
+            }
+        } else {
+            const f32x4 t0 = ld_f4(a.theta + base), t1 = ld_f4(a.theta + base + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                th[e] = t0[e];
+                th[4 + e] = t1[e];
+            }
+            if constexpr (UPDATE) {
+                const f32x4 v0 = ld_f4(a.momentum + base), v1 = ld_f4(a.momentum + base + 4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    v[e] = v0[e];
+                    v[4 + e] = v1[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const u32x4 w = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + base);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    r[k][2 * e] = bf16_lo(w[e]);
+                    r[k][2 * e + 1] = bf16_hi(w[e]);
+                }
+            }
+        }
+
+        float s[K], q[K], m = 0.f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
+        float th_new[V], v_new[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            float re[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) re[k] = r[k][e];
+            one_param<K, STATS, UPDATE>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e]);
+        }
+        if constexpr (STATS) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                acc[k] += (double)s[k];
+                acc[K + k] += (double)q[k];
+            }
+            acc[2 * K] += (double)m;
+        }
+        if constexpr (UPDATE) {
+            if constexpr (RT == RT_F32) {
+                st_f4(a.theta + base, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+                st_f4(a.momentum + base, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+                if constexpr (RESET) {
+                    const f32x4 o = {th_new[0], th_new[1], th_new[2], th_new[3]};
+#pragma unroll
+                    for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + base, o);
+                }
+            } else {
+                st_f4(a.theta + base, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+                st_f4(a.theta + base + 4, f32x4{th_new[4], th_new[5], th_new[6], th_new[7]});
+                st_f4(a.momentum + base, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+                st_f4(a.momentum + base + 4, f32x4{v_new[4], v_new[5], v_new[6], v_new[7]});
+                if constexpr (RESET) {
+                    const u32x4 o = {bf16_pack(th_new[0], th_new[1]), bf16_pack(th_new[2], th_new[3]),
+                                     bf16_pack(th_new[4], th_new[5]), bf16_pack(th_new[6], th_new[7])};
+#pragma unroll
+                    for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + base, o);
+                }
+            }
+        }
+    }
+
+    // Ragged tail: the last n mod V parameters, one per thread of workgroup 0.
+    const int64_t tail0 = nvec * V;
+    if (gtid < a.n - tail0) {
+        const int64_t j = tail0 + gtid;
+        const float th = a.theta[j];
+        const float v = UPDATE ? a.momentum[j] : 0.f;
+        float r[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if constexpr (RT == RT_F32)
+                r[k] = static_cast<const float*>(a.replicas[k])[j];
+            else
+                r[k] = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.replicas[k])[j] << 16);
+        }
+        float s[K], q[K], m = 0.f, th_new = 0.f, v_new = 0.f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
+        one_param<K, STATS, UPDATE>(th, v, r, a, s, q, m, th_new, v_new);
+        if constexpr (STATS) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                acc[k] += (double)s[k];
+                acc[K + k] += (double)q[k];
+            }
+            acc[2 * K] += (double)m;
+        }
+        if constexpr (UPDATE) {
+            a.theta[j] = th_new;
+            a.momentum[j] = v_new;
+            if constexpr (RESET) {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    if constexpr (RT == RT_F32)
+                        static_cast<float*>(a.replicas[k])[j] = th_new;
+                    else
+                        static_cast<uint16_t*>(a.replicas[k])[j] = (uint16_t)bf16_rne(th_new);
+                }
+            }
+        }
+    }
+
+    if constexpr (STATS) grid_reduce<NS>(acc, a);
+}
+
+// ------------------------------------------------------------ reset kernel --
+// theta_k <- theta for every replica.
+template <int K, int RT>
+__global__ void __launch_bounds__(kBlock) reset_kernel(RoundArgs a) {
+    constexpr int V = RT == RT_F32 ? 4 : 8;
+    const int64_t nvec = a.n / V;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (int64_t i = gtid; i < nvec; i += stride) {
+        const int64_t base = i * V;
+        if constexpr (RT == RT_F32) {
+            const f32x4 t = ld_f4(a.theta + base);
+#pragma unroll
+            for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + base, t);
+        } else {
+            const f32x4 t0 = ld_f4(a.theta + base), t1 = ld_f4(a.theta + base + 4);
+            const u32x4 o = {bf16_pack(t0[0], t0[1]), bf16_pack(t0[2], t0[3]), bf16_pack(t1[0], t1[1]),
+                             bf16_pack(t1[2], t1[3])};
+#pragma unroll
+            for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + base, o);
+        }
+    }
+    const int64_t tail0 = nvec * V;
+    if (gtid < a.n - tail0) {
+        const int64_t j = tail0 + gtid;
+        const float t = a.theta[j];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if constexpr (RT == RT_F32)
+                static_cast<float*>(a.replicas[k])[j] = t;
+            else
+                static_cast<uint16_t*>(a.replicas[k])[j] = (uint16_t)bf16_rne(t);
+        }
+    }
+}
+
+// Launchers, one per (replica type, mode) translation unit.
+typedef hipError_t (*RoundLauncher)(int k, int blocks, hipStream_t stream, const RoundArgs& a);
+hipError_t launch_round_f32_m0(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m1(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m2(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m3(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m4(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m0(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m1(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m2(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m3(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m4(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_reset(int rt, int k, int blocks, hipStream_t stream, const RoundArgs& a);
+
+}  // namespace autoloco

@@ -1,0 +1,247 @@
+"""CPU tests of the built library: it loads and exports every symbol the C
+header declares, and its host-side scalar code (schedule, learning-rate mass,
+outer correction, interval controller) takes exactly the oracle's values and
+decisions.  No device call is made here."""
+import math
+import os
+import re
+import warnings
+
+import pytest
+
+import paper_2609_36662_amd as al
+from oracle import controller as oc
+from oracle import correction as ocorr
+from tests.controller_driver import Event, drive
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "autoloco.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \*]*?\b(autoloco_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for must in ("autoloco_round_stats", "autoloco_outer_step", "autoloco_select_interval",
+                 "autoloco_broadcast_reset", "autoloco_create", "autoloco_outer_correction"):
+        assert must in names
+    assert len(names) >= 20
+
+
+def test_library_exports_every_declared_symbol():
+    lib = al.lib()
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    bound = {name for name, _, _ in al._lib.SYMBOLS}
+    assert set(_declared_functions()) <= bound, "binding misses a declared call"
+
+
+def test_status_strings():
+    lib = al.lib()
+    assert lib.autoloco_status_string(0) == b"ok"
+    assert lib.autoloco_status_string(-3) == b"device buffers overlap"
+
+
+# ------------------------------------------------------------ schedule
+SCHEDS = [ocorr.Schedule(), ocorr.Schedule(peak=5e-6, warmup=195, total=6490, min_lr=0.0),
+          ocorr.Schedule(peak=1e-3, min_lr=1e-4, warmup=0, total=1000)]
+
+
+def _csched(s):
+    return al.make_schedule(s.peak, s.min_lr, s.warmup, s.total)
+
+
+@pytest.mark.parametrize("si", range(len(SCHEDS)))
+def test_lr_and_mass_equal_oracle_bitwise(si):
+    s = SCHEDS[si]
+    cs = _csched(s)
+    for step in [0, 1, 194, 195, 999, 1000, 1001, 20_000, 49_999, 50_000, 70_000]:
+        assert al.autoloco_inner_lr(cs, step) == ocorr.inner_lr(s, step)
+    for start, steps in [(0, 500), (500, 500), (20_000, 75), (20_000, 50), (16_000, 750), (49_750, 250),
+                         (3_000, 0)]:
+        assert al.autoloco_lr_mass(cs, start, steps) == ocorr.lr_mass(s, start, steps)
+    assert math.isnan(al.autoloco_lr_mass(cs, -1, 3))
+
+
+@pytest.mark.parametrize("mu_base,normalize", [(0.9, False), (0.7, True)])
+def test_outer_correction_equals_oracle_bitwise(mu_base, normalize):
+    cfg = ocorr.OuterConfig(mu_base=mu_base, normalize=normalize)
+    ccfg = al.make_outer_cfg(mu_base=mu_base, normalize=normalize)
+    sched = ocorr.Schedule()
+    for h_sel, h_ref in [(75, 50), (750, 500), (1000, 500), (500, 500), (250, 500), (1500, 500)]:
+        lam = ocorr.lr_mass(sched, 20_000, h_sel)
+        lam_b = ocorr.lr_mass(sched, 20_000, h_ref)
+        o = ocorr.outer_correction(cfg, lam, lam_b)
+        c = al.autoloco_outer_correction(ccfg, lam, lam_b)
+        assert (c.rho, c.mu, c.kappa, c.eta_out, bool(c.normalize)) == (o.rho, o.mu, o.kappa, o.eta, o.normalize)
+
+
+def test_outer_correction_rejects_bad_config():
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_outer_correction(al.make_outer_cfg(mu_base=1.0), 1.0, 1.0)
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_outer_correction(al.make_outer_cfg(), float("nan"), 1.0)
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_outer_correction(al.make_outer_cfg(mu_min=0.95), 1.0, 1.0)
+
+
+# ---------------------------------------------------------- controller
+def _ccfg(cfg: oc.ControllerConfig):
+    s, o = cfg.sched, cfg.outer
+    return al.default_controller_cfg(
+        h_base=cfg.h_base, h_min=cfg.h_min, h_max=cfg.h_max, q_h=cfg.q_h,
+        budget_steps=cfg.budget_steps, beta_tok=cfg.beta_tok, eps=cfg.eps,
+        thr_cand=cfg.thr_cand, thr_mod=cfg.thr_mod, thr_sev=cfg.thr_sev,
+        cand_exposure=cfg.cand_exposure, retire_frac=cfg.retire_frac,
+        red_moderate=cfg.red_moderate, red_severe=cfg.red_severe, ref_ema=cfg.ref_ema,
+        mad_scale=cfg.mad_scale, scale_floor=cfg.scale_floor, n_mapper_boot=cfg.n_mapper_boot,
+        n_ref_boot=cfg.n_ref_boot, n_var=cfg.n_var, hist_max=cfg.hist_max,
+        moderate_confirm=cfg.moderate_confirm, fallback_count=cfg.fallback_count,
+        sched=_csched(s),
+        outer=al.make_outer_cfg(o.eta_base, o.mu_base, o.mu_min, o.mu_max, o.kappa_max, o.eps,
+                                o.normalize))
+
+
+def _same_float(a, b):
+    return (math.isnan(a) and math.isnan(b)) or a == b
+
+
+def _near_ties(cfg, decisions):
+    ties = []
+    for i, d in enumerate(decisions):
+        z = d.z_max
+        if not math.isnan(z):
+            for thr in (cfg.thr_cand, cfg.thr_mod, cfg.thr_sev):
+                if abs(z - thr) < 1e-6:
+                    ties.append((i, z, thr))
+    return ties
+
+
+def _replay(cfg: oc.ControllerConfig, observations, ref_decisions):
+    ctl = al.autoloco_controller_create(_ccfg(cfg))
+    got = [al.autoloco_select_interval(ctl, None)]
+    for o in observations:
+        got.append(al.autoloco_select_interval(
+            ctl, al.make_observation(o.D, o.C, o.lambda_done, o.tokens, o.h_step_done, o.finite)))
+    assert len(got) == len(ref_decisions)
+    for i, (g, r) in enumerate(zip(got, ref_decisions)):
+        fields = (g.start_step, g.h_tok, g.h_step, g.h_ref, g.assessment, g.phase, bool(g.done))
+        expect = (r.start_step, r.h_tok, r.h_step, r.h_ref, r.assessment, r.phase, r.done)
+        assert fields == expect, f"decision {i}: {fields} != {expect}"
+        assert g.lambda_sel == r.lambda_sel and g.lambda_base == r.lambda_base, i
+        assert _same_float(g.z_max, r.z_max), (i, g.z_max, r.z_max)
+        assert (g.coeffs.rho, g.coeffs.mu, g.coeffs.eta_out, g.coeffs.kappa) == \
+            (r.coeffs.rho, r.coeffs.mu, r.coeffs.eta, r.coeffs.kappa), i
+    return got
+
+
+SCENARIOS = {
+    "c4_all_supported": (oc.ControllerConfig(), {}),
+    "moderate_twice": (oc.ControllerConfig(h_max=500), {10: Event(loss=3e-3), 11: Event(loss=3e-3)}),
+    "severe": (oc.ControllerConfig(h_max=500), {10: Event(loss=5e-3)}),
+    "tie_750": (oc.ControllerConfig(h_base=750, h_max=750), {10: Event(loss=3e-3), 11: Event(loss=3e-3)}),
+    "nonfinite_fallback": (oc.ControllerConfig(h_max=500), {10: Event(nonfinite=True),
+                                                            11: Event(nonfinite=True)}),
+    "reject_and_retire": (oc.ControllerConfig(), {8: Event(loss=3e-3)}),
+    "midpoint": (oc.ControllerConfig(cand_exposure=1.5), {8: Event(loss=5e-3)}),
+    "cand2_adopt": (oc.ControllerConfig(), {8: Event(loss=2e-3)}),
+    "cand2_reject": (oc.ControllerConfig(), {8: Event(loss=2e-3), 9: Event(loss=3e-3)}),
+    "normalised_sft_like": (oc.ControllerConfig(h_base=100, h_min=50, h_max=150, q_h=10, budget_steps=6490,
+                                                sched=ocorr.Schedule(peak=5e-6, warmup=195, total=6490),
+                                                outer=ocorr.OuterConfig(mu_base=0.7, normalize=True)),
+                            {20: Event(loss=5e-3), 40: Event(nonfinite=True)}),
+    "mixed": (oc.ControllerConfig(), {8: Event(loss=2e-3), 20: Event(loss=3e-3), 21: Event(loss=3e-3),
+                                      30: Event(loss=6e-3), 31: Event(loss=6e-3), 45: Event(nonfinite=True)}),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SCENARIOS))
+def test_controller_matches_oracle_decision_by_decision(name):
+    cfg, script = SCENARIOS[name]
+    dens = None
+    if name == "mixed":
+        dens = lambda t: float(1 << 20) * (1.0 if t < 25 else 0.8)   # token density drop
+    decs, obs = drive(cfg, script, density=dens)
+    ties = _near_ties(cfg, decs)
+    if ties:
+        warnings.warn(f"near-tie z values in scenario {name}: {ties}")
+    _replay(cfg, obs, decs)
+
+
+def test_controller_reproduces_c4_trajectory():
+    ctl = al.autoloco_controller_create()
+    cfg = oc.ControllerConfig()
+    sched = _csched(cfg.sched)
+    d = al.autoloco_select_interval(ctl, None)
+    seq = []
+    while not d.done:
+        seq.append(d.h_step)
+        lam = al.autoloco_lr_mass(sched, d.start_step, d.h_step)
+        d_ref, c_ref, l_ref = al.autoloco_controller_reference(ctl)
+        if d_ref > 0:
+            xi = lam / (l_ref + cfg.eps)
+            D, Cc = d_ref * xi * xi, c_ref
+        else:
+            D, Cc = (10.0 * lam) ** 2, 5.0
+        d = al.autoloco_select_interval(ctl, al.make_observation(D, Cc, lam, float(1 << 20) * d.h_step,
+                                                                  d.h_step))
+    runs = []
+    for h in seq:
+        if runs and runs[-1][0] == h:
+            runs[-1][1] += 1
+        else:
+            runs.append([h, 1])
+    assert [tuple(r) for r in runs] == [(500, 7), (550, 5), (600, 5), (650, 5), (700, 5), (750, 45), (250, 1)]
+    with pytest.raises(al.AutolocoError) as e:
+        al.autoloco_select_interval(ctl, al.make_observation(1, 1, 1, 1, 1))
+    assert e.value.status == -6
+
+
+def test_controller_call_order_errors():
+    ctl = al.autoloco_controller_create()
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_select_interval(ctl, al.make_observation(1, 1, 1, 1, 1))   # first call takes none
+    al.autoloco_select_interval(ctl, None)
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_select_interval(ctl, None)                                  # later calls need one
+
+
+def test_controller_rejects_bad_config():
+    for bad in (dict(q_h=0), dict(h_min=800), dict(hist_max=17), dict(n_ref_boot=0),
+                dict(thr_cand=3.0), dict(red_severe=1.0)):
+        with pytest.raises(al.AutolocoError):
+            al.autoloco_controller_create(al.default_controller_cfg(**bad))
+
+
+def test_controller_checkpoint_resume_is_bitwise():
+    cfg, script = SCENARIOS["mixed"]
+    decs, obs = drive(cfg, script)
+    cobs = [al.make_observation(o.D, o.C, o.lambda_done, o.tokens, o.h_step_done, o.finite) for o in obs]
+
+    def fields(d):
+        return (d.start_step, d.h_tok, d.h_step, d.h_ref, d.lambda_sel, d.lambda_base, d.assessment,
+                d.phase, d.done, d.coeffs.mu, d.coeffs.eta_out, d.coeffs.rho)
+
+    straight = al.autoloco_controller_create(_ccfg(cfg))
+    ref = [fields(al.autoloco_select_interval(straight, None))]
+    ref += [fields(al.autoloco_select_interval(straight, o)) for o in cobs[:40]]
+
+    first = al.autoloco_controller_create(_ccfg(cfg))
+    got = [fields(al.autoloco_select_interval(first, None))]
+    got += [fields(al.autoloco_select_interval(first, o)) for o in cobs[:20]]
+    blob = al.autoloco_controller_save(first)
+    first.close()
+    resumed = al.autoloco_controller_create()          # a different configuration: the saved one wins
+    al.autoloco_controller_load(resumed, blob)
+    got += [fields(al.autoloco_select_interval(resumed, o)) for o in cobs[20:40]]
+    assert got == ref
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_controller_load(resumed, blob[:-8])
+    bad = bytearray(blob)
+    bad[0] ^= 0xFF
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_controller_load(resumed, bytes(bad))
