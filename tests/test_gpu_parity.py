@@ -11,7 +11,7 @@ import torch
 import paper_2609_36662_amd as al
 from oracle import correction as ocorr
 from oracle import round as orr
-from tests.gpu_common import (assert_close_elementwise, assert_stats_close, bf16_ulp_distance, bits16,
+from tests.gpu_common import (assert_bf16_reset_close, assert_close_elementwise, assert_stats_close, bits16,
                               cpu_inputs, host_array, to_device)
 from workloads import drift
 
@@ -59,11 +59,10 @@ def _check_full_round(ctx, n, k, replica_dtype=torch.float32, normalize=False, s
             assert np.array_equal(r.cpu().numpy().view(np.uint32), th.view(np.uint32))
     else:
         mine = bits16(dev.theta.to(torch.bfloat16))      # torch's own rounding of the GPU theta'
-        oracle_bits = orr.to_bf16_bits(ref.theta)
         for r in dev.replicas:
             rb = bits16(r)
             assert np.array_equal(rb, mine)
-            assert int(bf16_ulp_distance(rb, oracle_bits).max()) <= 1
+            assert_bf16_reset_close(rb, ref.theta)
     return st, ref
 
 
