@@ -150,7 +150,7 @@ def main() -> int:
     ctx = al.autoloco_create(0)
     if args.grid:
         al.autoloco_set_grid_limit(ctx, args.grid)
-    blocks, threads = al.autoloco_launch_shape(ctx, n, al.F32 if rdt == "f32" else al.BF16)
+    blocks, threads = al.autoloco_launch_shape(ctx, n, k, al.F32 if rdt == "f32" else al.BF16)
     al.autoloco_set_timing(ctx, True)
     flags = al.FUSE_STATS | al.FUSE_RESET
 

@@ -87,12 +87,15 @@ const char* autoloco_last_error(const autoloco_ctx* ctx);
 int autoloco_set_timing(autoloco_ctx* ctx, int enable);
 /* Device milliseconds of the last timed launch; waits for it to finish. */
 int autoloco_last_kernel_ms(autoloco_ctx* ctx, float* ms);
-/* Cap on the number of workgroups of the streaming kernels (0 = the default,
- * a fixed multiple of the device's compute units).  The statistics are
- * bit-identical between runs with the same n, k and cap. */
+/* Cap on the number of workgroups of the streaming kernels, 0..16384 (0 = the
+ * default: one wave of resident workgroups of the fused kernel, i.e. compute
+ * units x workgroups per unit at that kernel's register use).  The statistics
+ * are bit-identical between runs with the same n, k, replica type, device and
+ * cap, and between the standalone and the fused call. */
 int autoloco_set_grid_limit(autoloco_ctx* ctx, int max_blocks);
-/* Workgroups and threads per workgroup a round over n parameters uses. */
-int autoloco_launch_shape(const autoloco_ctx* ctx, int64_t n, int32_t replica_dtype,
+/* Workgroups and threads per workgroup a round over n parameters with k
+ * replicas of the given type uses. */
+int autoloco_launch_shape(const autoloco_ctx* ctx, int64_t n, int32_t k, int32_t replica_dtype,
                           int32_t* blocks, int32_t* threads);
 
 /* ------------------------------------------------------------------------ */

@@ -107,7 +107,7 @@ SYMBOLS = [
     ("autoloco_set_timing", C.c_int, [C.c_void_p, C.c_int]),
     ("autoloco_last_kernel_ms", C.c_int, [C.c_void_p, C.POINTER(C.c_float)]),
     ("autoloco_set_grid_limit", C.c_int, [C.c_void_p, C.c_int]),
-    ("autoloco_launch_shape", C.c_int, [C.c_void_p, C.c_int64, C.c_int32, C.POINTER(C.c_int32),
+    ("autoloco_launch_shape", C.c_int, [C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.POINTER(C.c_int32),
                                         C.POINTER(C.c_int32)]),
     ("autoloco_round_stats", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.c_double, C.POINTER(Stats)]),
     ("autoloco_outer_step", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
@@ -216,9 +216,9 @@ def autoloco_set_grid_limit(ctx: Context, max_blocks: int) -> None:
     _check(lib().autoloco_set_grid_limit(ctx.handle, int(max_blocks)), "autoloco_set_grid_limit", ctx)
 
 
-def autoloco_launch_shape(ctx: Context, n: int, replica_dtype: int = F32):
+def autoloco_launch_shape(ctx: Context, n: int, k: int, replica_dtype: int = F32):
     b, t = C.c_int32(), C.c_int32()
-    _check(lib().autoloco_launch_shape(ctx.handle, int(n), int(replica_dtype), C.byref(b), C.byref(t)),
+    _check(lib().autoloco_launch_shape(ctx.handle, int(n), int(k), int(replica_dtype), C.byref(b), C.byref(t)),
            "autoloco_launch_shape", ctx)
     return b.value, t.value
 

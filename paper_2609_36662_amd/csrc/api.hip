@@ -16,7 +16,6 @@ using namespace autoloco;
 
 namespace {
 
-constexpr int kBlocksPerCu = 8;     // default grid: 8 workgroups of 256 per compute unit
 constexpr int kMaxBlocks = 16384;   // scratch sized for this many workgroups
 
 }  // namespace
@@ -26,6 +25,7 @@ struct autoloco_ctx {
     hipStream_t stream = nullptr;
     int num_cus = 0;
     int grid_limit = 0;
+    int occupancy[2][AUTOLOCO_MAX_K + 1] = {};  // resident workgroups per CU, by replica type and k
     double* partials = nullptr;
     unsigned int* ticket = nullptr;
     double* sums = nullptr;
@@ -63,10 +63,17 @@ int hip_fail(autoloco_ctx* ctx, hipError_t e, const char* what) {
 
 size_t replica_size(int32_t dtype) { return dtype == AUTOLOCO_BF16 ? 2 : 4; }
 
-int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype) {
+// Default grid: exactly one wave of resident workgroups of the fused kernel
+// (compute units x workgroups that fit per unit).  A larger grid leaves a
+// partial last wave; a smaller one leaves units idle.  Every mode of a given
+// (k, replica type) uses the same grid, so the statistics of a standalone
+// call and of a fused call are summed in the same order, bit for bit.
+int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k) {
     const int64_t v = dtype == AUTOLOCO_BF16 ? 8 : 4;
     const int64_t nvec = n / v;
-    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * kBlocksPerCu;
+    int per_cu = ctx->occupancy[dtype == AUTOLOCO_BF16 ? 1 : 0][k];
+    if (per_cu < 1) per_cu = 1;
+    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * per_cu;
     if (limit > kMaxBlocks) limit = kMaxBlocks;
     int64_t want = (nvec + kBlock - 1) / kBlock;
     if (want < 1) want = 1;
@@ -163,7 +170,7 @@ RoundArgs make_args(autoloco_ctx* ctx, const autoloco_buffers* b) {
 // sums and fills *out.
 int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, int mode, bool stats,
               double eps, autoloco_stats* out) {
-    const int blocks = blocks_for(ctx, b->n, b->replica_dtype);
+    const int blocks = blocks_for(ctx, b->n, b->replica_dtype, b->k);
     hipError_t e;
     if (ctx->timing && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
@@ -210,6 +217,10 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
         return AUTOLOCO_E_DEVICE;
     }
     c->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+    for (int k = 1; k <= AUTOLOCO_MAX_K; ++k) {
+        c->occupancy[0][k] = occupancy_round_f32_m4(k);
+        c->occupancy[1][k] = occupancy_round_bf16_m4(k);
+    }
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
               hipMalloc(&c->ticket, 256) == hipSuccess &&
               hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
@@ -268,10 +279,12 @@ int autoloco_set_grid_limit(autoloco_ctx* c, int max_blocks) {
     return AUTOLOCO_OK;
 }
 
-int autoloco_launch_shape(const autoloco_ctx* c, int64_t n, int32_t dtype, int32_t* blocks, int32_t* threads) {
+int autoloco_launch_shape(const autoloco_ctx* c, int64_t n, int32_t k, int32_t dtype, int32_t* blocks,
+                          int32_t* threads) {
     if (c == nullptr || blocks == nullptr || threads == nullptr || n < 0) return AUTOLOCO_E_INVALID;
     if (dtype != AUTOLOCO_F32 && dtype != AUTOLOCO_BF16) return AUTOLOCO_E_INVALID;
-    *blocks = blocks_for(c, n, dtype);
+    if (k < 1 || k > AUTOLOCO_MAX_K) return AUTOLOCO_E_INVALID;
+    *blocks = blocks_for(c, n, dtype, k);
     *threads = kBlock;
     return AUTOLOCO_OK;
 }
@@ -325,7 +338,7 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
-    const int blocks = blocks_for(c, b->n, b->replica_dtype);
+    const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k);
     hipError_t e;
     if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);

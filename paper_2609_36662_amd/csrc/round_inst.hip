@@ -9,6 +9,7 @@
 
 #define AL_CAT(a, b, c) a##b##_m##c
 #define AL_NAME(rt, m) AL_CAT(launch_round_, rt, m)
+#define AL_OCC_NAME(rt, m) AL_CAT(occupancy_round_, rt, m)
 
 namespace autoloco {
 namespace {
@@ -24,7 +25,38 @@ hipError_t launch_k(int blocks, hipStream_t stream, const RoundArgs& a) {
     return hipGetLastError();
 }
 
+template <int K>
+int occ_k() {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, round_kernel<K, AL_RT, kStats, kUpdate, kReset>, kBlock,
+                                                     0) != hipSuccess)
+        return 0;
+    return blocks;
+}
+
 }  // namespace
+
+int AL_OCC_NAME(AL_RTNAME, AL_MODE)(int k) {
+    switch (k) {
+        case 1: return occ_k<1>();
+        case 2: return occ_k<2>();
+        case 3: return occ_k<3>();
+        case 4: return occ_k<4>();
+        case 5: return occ_k<5>();
+        case 6: return occ_k<6>();
+        case 7: return occ_k<7>();
+        case 8: return occ_k<8>();
+        case 9: return occ_k<9>();
+        case 10: return occ_k<10>();
+        case 11: return occ_k<11>();
+        case 12: return occ_k<12>();
+        case 13: return occ_k<13>();
+        case 14: return occ_k<14>();
+        case 15: return occ_k<15>();
+        case 16: return occ_k<16>();
+        default: return 0;
+    }
+}
 
 hipError_t AL_NAME(AL_RTNAME, AL_MODE)(int k, int blocks, hipStream_t stream, const RoundArgs& a) {
     switch (k) {

@@ -380,5 +380,8 @@ hipError_t launch_round_bf16_m2(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m3(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m4(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_reset(int rt, int k, int blocks, hipStream_t stream, const RoundArgs& a);
+// Resident workgroups per compute unit of the fused (update + stats + reset) kernel.
+int occupancy_round_f32_m4(int k);
+int occupancy_round_bf16_m4(int k);
 
 }  // namespace autoloco
