@@ -101,6 +101,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama-1.1b", choices=sorted(WORKLOADS))
     ap.add_argument("--grid", type=int, default=0, help="cap on workgroups (0 = library default)")
+    ap.add_argument("--k", type=int, default=0, help="override the workload's replica count")
+    ap.add_argument("--alloc", choices=("spread", "torch"), default="spread",
+                    help="spread: the library's placement-aware allocator; torch: torch.empty")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--cpu-sample", type=int, default=1 << 22)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -118,6 +121,8 @@ def main() -> int:
     from workloads import drift, shapes
 
     shape_name, k, rdt, recipe_name, h_sel, h_base = WORKLOADS[args.workload]
+    if args.k:
+        k = args.k
     n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
     recipe = drift.MIXED if recipe_name == "mixed" else drift.spread_recipe(1e-3)
     tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
@@ -133,10 +138,19 @@ def main() -> int:
     coeffs = al.autoloco_outer_correction(al.make_outer_cfg(), lam, lam_b)
 
     log(f"workload {args.workload}: n={n:,} K={k} replicas={rdt} bytes/round={bytes_per_round/1e9:.3f} GB")
+    ctx = al.autoloco_create(0)
     t = time.perf_counter()
-    inp = drift.make_round_inputs(n, k, seed=42, recipe=recipe, replica_dtype=tdtype, device=dev)
+    spread = False
+    if args.alloc == "spread":
+        ts, spread = al.spread_tensors(ctx, n, [torch.float32, torch.float32] + [tdtype] * k)
+        inp = drift.RoundInputs(ts[0], ts[1], ts[2:])
+    else:
+        inp = drift.empty_inputs(n, k, replica_dtype=tdtype, device=dev)
+    drift.fill_theta_momentum(inp, seed=42, recipe=recipe)
+    drift.fill_replicas(inp, seed=42, recipe=recipe)
     torch.cuda.synchronize()
-    log(f"inputs generated in {time.perf_counter() - t:.1f} s")
+    log(f"buffers ({args.alloc}{', spread' if spread else ''}) allocated and inputs generated in "
+        f"{time.perf_counter() - t:.1f} s")
 
     sample = None
     if not args.no_cpu_baseline:
@@ -147,7 +161,6 @@ def main() -> int:
             return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
         sample = (host(inp.theta), host(inp.momentum), [host(r) for r in inp.replicas], rdt)
 
-    ctx = al.autoloco_create(0)
     if args.grid:
         al.autoloco_set_grid_limit(ctx, args.grid)
     blocks, threads = al.autoloco_launch_shape(ctx, n, k, al.F32 if rdt == "f32" else al.BF16)
@@ -205,7 +218,6 @@ def main() -> int:
         del src, dst
         log(f"device-to-device copy of 4 GiB: {ceiling:.0f} GB/s")
 
-    ctx.close()
     mean_ms = statistics.mean(kernel_ms)
     achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
     tag = f"round_{rdt}_k{k}_{args.workload}"
@@ -233,7 +245,8 @@ def main() -> int:
             "workload": f"{args.workload}: {n:,} parameters as one flat arena per buffer, K={k} "
                         f"{rdt} replicas, fp32 theta and momentum, fused stats + Nesterov + reset",
             "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
-            "grid": [blocks, threads], "h_selected": h_sel, "h_base": h_base,
+            "grid": [blocks, threads], "alloc": args.alloc + (" (spread)" if spread else ""),
+            "h_selected": h_sel, "h_base": h_base,
             "rho": coeffs.rho, "mu": coeffs.mu, "eta_out": coeffs.eta_out,
         },
         "roofline": {
@@ -250,6 +263,10 @@ def main() -> int:
         "kernel_source_sha256_16": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
+    del inp
+    if args.alloc == "spread":
+        del ts
+    ctx.close()
     return 0
 
 

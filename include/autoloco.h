@@ -99,6 +99,27 @@ int autoloco_launch_shape(const autoloco_ctx* ctx, int64_t n, int32_t k, int32_t
                           int32_t* blocks, int32_t* threads);
 
 /* ------------------------------------------------------------------------ */
+/* Placement of the streamed buffers                                         */
+/* ------------------------------------------------------------------------ */
+
+/* Allocates `count` device buffers of `bytes` each (16-byte aligned, not
+ * overlapping) for buffers that one kernel streams through at the same time,
+ * such as theta, the momentum and the k replicas of a round, placed far apart
+ * in the device's physical memory.  On MI355X, streams whose pages lie close
+ * together in physical memory collide in the DRAM address mapping: the round's
+ * ten concurrent streams (k = 8) run at ~5.1 TB/s when adjacent and at
+ * ~6.2 TB/s when spread over the device.  The call fills the free device
+ * memory (leaving headroom) with equal slots, keeps `count` slots evenly spaced
+ * among them and frees the rest before returning, so other allocations made at
+ * the same time may fail transiently; call it at set-up.  With too little free
+ * memory to spread, it allocates plainly.  *spread (may be NULL) reports
+ * which.  Each buffer is freed with autoloco_free.
+ * Errors: E_INVALID (null pointers, count outside 1..64, bytes == 0), E_NOMEM. */
+int autoloco_alloc_spread(autoloco_ctx* ctx, int32_t count, size_t bytes, void** out, int32_t* spread);
+/* Frees one buffer from autoloco_alloc_spread (NULL is a no-op). */
+int autoloco_free(autoloco_ctx* ctx, void* ptr);
+
+/* ------------------------------------------------------------------------ */
 /* Device buffers of one round                                               */
 /* ------------------------------------------------------------------------ */
 

@@ -109,6 +109,9 @@ SYMBOLS = [
     ("autoloco_set_grid_limit", C.c_int, [C.c_void_p, C.c_int]),
     ("autoloco_launch_shape", C.c_int, [C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.POINTER(C.c_int32),
                                         C.POINTER(C.c_int32)]),
+    ("autoloco_alloc_spread", C.c_int, [C.c_void_p, C.c_int32, C.c_size_t, C.POINTER(C.c_void_p),
+                                        C.POINTER(C.c_int32)]),
+    ("autoloco_free", C.c_int, [C.c_void_p, C.c_void_p]),
     ("autoloco_round_stats", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.c_double, C.POINTER(Stats)]),
     ("autoloco_outer_step", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                       C.c_uint32, C.c_double, C.POINTER(Stats)]),
@@ -221,6 +224,71 @@ def autoloco_launch_shape(ctx: Context, n: int, k: int, replica_dtype: int = F32
     _check(lib().autoloco_launch_shape(ctx.handle, int(n), int(k), int(replica_dtype), C.byref(b), C.byref(t)),
            "autoloco_launch_shape", ctx)
     return b.value, t.value
+
+
+# -------------------------------------------------------------- placement --
+_TYPESTR = {"float32": "<f4", "bfloat16": "<V2"}
+
+
+class _DeviceBuffer:
+    """Owner of one autoloco_alloc_spread buffer; exposes it to torch through
+    __cuda_array_interface__ and frees it when the last view is gone."""
+
+    def __init__(self, ctx: "Context", ptr: int, nbytes: int):
+        self._ctx = ctx
+        self.ptr = ptr
+        self.nbytes = nbytes
+
+    def view(self, n: int, dtype):
+        import torch
+        if dtype == torch.float32:
+            cai = {"shape": (n,), "typestr": "<f4", "data": (self.ptr, False), "version": 2, "strides": None}
+            holder = type("_Cai", (), {})()
+            holder.__cuda_array_interface__ = cai
+            holder.owner = self
+            return torch.as_tensor(holder, device=f"cuda:{self._ctx.device}")
+        if dtype == torch.bfloat16:
+            # bf16 has no array-interface type string: view the bytes as int16, then reinterpret
+            cai = {"shape": (n,), "typestr": "<i2", "data": (self.ptr, False), "version": 2, "strides": None}
+            holder = type("_Cai", (), {})()
+            holder.__cuda_array_interface__ = cai
+            holder.owner = self
+            return torch.as_tensor(holder, device=f"cuda:{self._ctx.device}").view(torch.bfloat16)
+        raise TypeError(dtype)
+
+    def __del__(self):
+        try:
+            if self.ptr and self._ctx.handle:
+                lib().autoloco_free(self._ctx.handle, C.c_void_p(self.ptr))
+        except Exception:
+            pass
+        self.ptr = 0
+
+
+def autoloco_alloc_spread(ctx: "Context", count: int, nbytes: int):
+    """Raw pointers of `count` buffers of `nbytes`, spread in physical memory,
+    and whether spreading was possible."""
+    out = (C.c_void_p * count)()
+    spread = C.c_int32(0)
+    _check(lib().autoloco_alloc_spread(ctx.handle, int(count), int(nbytes), out, C.byref(spread)),
+           "autoloco_alloc_spread", ctx)
+    return [int(p) for p in out], bool(spread.value)
+
+
+def autoloco_free(ctx: "Context", ptr: int) -> None:
+    _check(lib().autoloco_free(ctx.handle, C.c_void_p(ptr)), "autoloco_free", ctx)
+
+
+def spread_tensors(ctx: "Context", n: int, dtypes):
+    """torch tensors of n elements each (one per dtype in `dtypes`), backed by
+    autoloco_alloc_spread memory; each frees its memory when collected."""
+    import torch
+    sizes = [n * (4 if d == torch.float32 else 2) for d in dtypes]
+    ptrs, spread = autoloco_alloc_spread(ctx, len(dtypes), max(max(sizes), 16))
+    out = []
+    for p, d, nb in zip(ptrs, dtypes, sizes):
+        out.append(_DeviceBuffer(ctx, p, nb).view(n, d))
+    return out, spread
 
 
 # ----------------------------------------------------------- marshalling --

@@ -8,6 +8,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "autoloco.h"
 #include "round_kernels.hpp"
@@ -348,6 +349,68 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
         c->timed_valid = true;
     }
     c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+int autoloco_alloc_spread(autoloco_ctx* c, int32_t count, size_t bytes, void** out, int32_t* spread) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (out == nullptr || count < 1 || count > 64 || bytes == 0)
+        return fail(c, AUTOLOCO_E_INVALID, "alloc_spread: need out, 1 <= count <= 64, bytes > 0");
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    const size_t gran = size_t(2) << 20;
+    const size_t slot = (bytes + gran - 1) / gran * gran;
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) return fail(c, AUTOLOCO_E_DEVICE, "hipMemGetInfo failed");
+    size_t reserve = total_b / 64;
+    if (reserve < (size_t(2) << 30)) reserve = size_t(2) << 30;
+    size_t want = free_b > reserve ? (free_b - reserve) / slot : 0;
+    if (want > 1024) want = 1024;
+    if (spread) *spread = 0;
+    if (want < size_t(2) * count) {
+        // not enough room to spread: plain allocations
+        for (int i = 0; i < count; ++i) {
+            if (hipMalloc(&out[i], slot) != hipSuccess) {
+                for (int j = 0; j < i; ++j) (void)hipFree(out[j]);
+                return fail(c, AUTOLOCO_E_NOMEM, "alloc_spread: hipMalloc failed");
+            }
+        }
+        return AUTOLOCO_OK;
+    }
+    // Fill the free memory with equal slots in allocation order, keep an even
+    // selection of them, and return the others.
+    std::vector<void*> slots;
+    slots.reserve(want);
+    for (size_t i = 0; i < want; ++i) {
+        void* p = nullptr;
+        if (hipMalloc(&p, slot) != hipSuccess) break;
+        slots.push_back(p);
+    }
+    (void)hipGetLastError();  // a failed probe allocation is expected near the end
+    const size_t m = slots.size();
+    if (m < size_t(count)) {
+        for (void* p : slots) (void)hipFree(p);
+        return fail(c, AUTOLOCO_E_NOMEM, "alloc_spread: not enough device memory");
+    }
+    std::vector<char> keep(m, 0);
+    for (int i = 0; i < count; ++i) {
+        const size_t idx = count == 1 ? m / 2 : (size_t)((double)i * (double)(m - 1) / (double)(count - 1) + 0.5);
+        keep[idx] = 1;
+        out[i] = slots[idx];
+    }
+    for (size_t i = 0; i < m; ++i)
+        if (!keep[i]) (void)hipFree(slots[i]);
+    if (spread) *spread = m >= size_t(2) * count ? 1 : 0;
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+int autoloco_free(autoloco_ctx* c, void* ptr) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (ptr == nullptr) return AUTOLOCO_OK;
+    DeviceGuard g(c->device);
+    const hipError_t e = hipFree(ptr);
+    if (e != hipSuccess) return hip_fail(c, e, "hipFree");
     return AUTOLOCO_OK;
 }
 
