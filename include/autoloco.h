@@ -180,6 +180,26 @@ int autoloco_outer_step(autoloco_ctx* ctx, const autoloco_buffers* bufs,
                         const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
                         autoloco_stats* out);
 
+/* The same corrected Nesterov step, with the worker average taken through the
+ * INT8 blockwise pseudo-gradient codec of App. G.1 ("Low-precision
+ * communication configuration"): every Delta_k is encoded per block of 4,096
+ * parameters (FP32 scale = max|Delta_k| / 127, 1 for a zero block and at
+ * least 2^-126; codes round-to-nearest-even, clipped to +-127), decoded in
+ * FP32, averaged (float64 sum in worker order times 1/K, rounded once to
+ * FP32), and the mean is encoded and decoded once more; the step uses that
+ * decoded aggregate.  Statistics (FUSE_STATS): sq_norm from the
+ * pre-quantisation Delta_k (D), sq_mean from the decoded aggregate (C),
+ * sq_dev = ||Delta_k - aggregate||^2.  Blocks run over the flat buffer; the
+ * last one is shorter.  mean_codes ([n] int8) and mean_scales
+ * ([ceil(n / 4096)] fp32) receive the encoded mean, the payload every worker
+ * would receive; pass both or neither (NULL).  Non-finite data propagates and
+ * is reported as finite = 0; the codes of such blocks are unspecified.
+ * Errors: as autoloco_outer_step, plus E_INVALID for only one payload buffer,
+ * E_ALIGN / E_ALIAS for the payload buffers. */
+int autoloco_outer_step_int8(autoloco_ctx* ctx, const autoloco_buffers* bufs,
+                             const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
+                             autoloco_stats* out, int8_t* mean_codes, float* mean_scales);
+
 /* Replica reset alone: theta_k <- theta for every replica (Alg. "AutoLoCo
  * outer interval", start of the local loop).  Asynchronous on the stream.
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */

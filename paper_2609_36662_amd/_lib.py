@@ -115,6 +115,8 @@ SYMBOLS = [
     ("autoloco_round_stats", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.c_double, C.POINTER(Stats)]),
     ("autoloco_outer_step", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                       C.c_uint32, C.c_double, C.POINTER(Stats)]),
+    ("autoloco_outer_step_int8", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
+                                           C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p, C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_inner_lr", C.c_double, [C.POINTER(Schedule), C.c_int64]),
     ("autoloco_lr_mass", C.c_double, [C.POINTER(Schedule), C.c_int64, C.c_int64]),
@@ -353,6 +355,31 @@ def autoloco_outer_step(ctx: Context, theta, momentum, replicas, coeffs: OuterCo
     _check(lib().autoloco_outer_step(ctx.handle, C.byref(b), C.byref(coeffs), flags, eps,
                                      C.byref(out) if flags & FUSE_STATS else None),
            "autoloco_outer_step", ctx)
+    return out if flags & FUSE_STATS else None
+
+
+def autoloco_outer_step_int8(ctx: Context, theta, momentum, replicas, coeffs: OuterCoeffs,
+                             flags: int = FUSE_STATS | FUSE_RESET, eps: float = 1e-12, n=None,
+                             mean_codes=None, mean_scales=None) -> Optional[Stats]:
+    """The corrected step with the worker average taken through the INT8 codec."""
+    import torch
+    b = make_buffers(theta, replicas, momentum, n)
+    if (mean_codes is None) != (mean_scales is None):
+        raise ValueError("pass both payload buffers or neither")
+    if mean_codes is not None:
+        if mean_codes.dtype != torch.int8 or mean_scales.dtype != torch.float32:
+            raise TypeError("mean_codes must be int8 and mean_scales float32")
+        if mean_codes.device.type != "cuda" or mean_scales.device.type != "cuda":
+            raise TypeError("payload buffers must be device tensors")
+        nb = (b.n + 4095) // 4096
+        if mean_codes.numel() < b.n or mean_scales.numel() < nb:
+            raise ValueError("payload buffers too short")
+    out = Stats()
+    _check(lib().autoloco_outer_step_int8(ctx.handle, C.byref(b), C.byref(coeffs), flags, eps,
+                                          C.byref(out) if flags & FUSE_STATS else None,
+                                          C.c_void_p(mean_codes.data_ptr()) if mean_codes is not None else None,
+                                          C.c_void_p(mean_scales.data_ptr()) if mean_scales is not None else None),
+           "autoloco_outer_step_int8", ctx)
     return out if flags & FUSE_STATS else None
 
 

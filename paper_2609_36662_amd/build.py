@@ -54,6 +54,12 @@ def jobs():
             obj = os.path.join(BUILD, f"round_{rtname}_m{mode}.o")
             cmds.append([hipcc, *HIP_FLAGS, f"-DAL_RT={rt}", f"-DAL_RTNAME={rtname}", f"-DAL_MODE={mode}",
                          "-c", os.path.join(CSRC, "round_inst.hip"), "-o", obj])
+    for rt, rtname in ((0, "f32"), (1, "bf16")):
+        for st in (0, 1):
+            for rs in (0, 1):
+                obj = os.path.join(BUILD, f"int8_{rtname}_s{st}r{rs}.o")
+                cmds.append([hipcc, *HIP_FLAGS, f"-DAL_RT={rt}", f"-DAL_RTNAME={rtname}", f"-DAL_STATS={st}",
+                             f"-DAL_RESET={rs}", "-c", os.path.join(CSRC, "int8_inst.hip"), "-o", obj])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "api.hip"), "-o", os.path.join(BUILD, "api.o")])
     for src in ("scalar.cpp", "controller.cpp"):
         cmds.append(["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, src),

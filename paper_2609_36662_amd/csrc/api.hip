@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "autoloco.h"
+#include "int8_kernels.hpp"
 #include "round_kernels.hpp"
 
 using namespace autoloco;
@@ -27,6 +28,7 @@ struct autoloco_ctx {
     int num_cus = 0;
     int grid_limit = 0;
     int occupancy[2][AUTOLOCO_MAX_K + 1] = {};  // resident workgroups per CU, by replica type and k
+    int occupancy_int8[2][AUTOLOCO_MAX_K + 1] = {};
     double* partials = nullptr;
     unsigned int* ticket = nullptr;
     double* sums = nullptr;
@@ -221,6 +223,8 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
     for (int k = 1; k <= AUTOLOCO_MAX_K; ++k) {
         c->occupancy[0][k] = occupancy_round_f32_m4(k);
         c->occupancy[1][k] = occupancy_round_bf16_m4(k);
+        c->occupancy_int8[0][k] = occupancy_int8_f32_s1r1(k);
+        c->occupancy_int8[1][k] = occupancy_int8_bf16_s1r1(k);
     }
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
               hipMalloc(&c->ticket, 256) == hipSuccess &&
@@ -330,6 +334,90 @@ int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autolo
     const int mode = stats ? (reset ? MODE_UPDATE_STATS_RESET : MODE_UPDATE_STATS)
                            : (reset ? MODE_UPDATE_RESET : MODE_UPDATE);
     return run_round(c, b, a, mode, stats, eps, out);
+}
+
+int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
+                             uint32_t flags, double eps, autoloco_stats* out, int8_t* codes, float* scales) {
+    int st = validate(c, b, true);
+    if (st != AUTOLOCO_OK) return st;
+    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
+    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
+    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
+    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
+    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
+    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
+        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    if ((codes == nullptr) != (scales == nullptr))
+        return fail(c, AUTOLOCO_E_INVALID, "pass both payload buffers or neither");
+    if (b->n == 0) {
+        if (stats) zero_stats(b->k, eps, out);
+        return AUTOLOCO_OK;
+    }
+    const int64_t nblocks = (b->n + kCodecBlock - 1) / kCodecBlock;
+    if (codes != nullptr) {
+        const uintptr_t cp = reinterpret_cast<uintptr_t>(codes), sp = reinterpret_cast<uintptr_t>(scales);
+        if (cp % 16 != 0 || sp % 16 != 0) return fail(c, AUTOLOCO_E_ALIGN, "payload buffers not 16-byte aligned");
+        const uintptr_t c_hi = cp + static_cast<uintptr_t>(b->n), s_hi = sp + static_cast<uintptr_t>(nblocks) * 4u;
+        if (cp < s_hi && sp < c_hi) return fail(c, AUTOLOCO_E_ALIAS, "payload buffers overlap");
+        const uintptr_t fb = static_cast<uintptr_t>(b->n) * 4u, rb = static_cast<uintptr_t>(b->n) * replica_size(b->replica_dtype);
+        uintptr_t lo[AUTOLOCO_MAX_K + 2], hi[AUTOLOCO_MAX_K + 2];
+        int nr = 0;
+        lo[nr] = reinterpret_cast<uintptr_t>(b->theta); hi[nr] = lo[nr] + fb; ++nr;
+        lo[nr] = reinterpret_cast<uintptr_t>(b->momentum); hi[nr] = lo[nr] + fb; ++nr;
+        for (int k = 0; k < b->k; ++k) {
+            lo[nr] = reinterpret_cast<uintptr_t>(b->replicas[k]);
+            hi[nr] = lo[nr] + rb;
+            ++nr;
+        }
+        for (int i = 0; i < nr; ++i)
+            if ((cp < hi[i] && lo[i] < c_hi) || (sp < hi[i] && lo[i] < s_hi))
+                return fail(c, AUTOLOCO_E_ALIAS, "payload buffers overlap a round buffer");
+    }
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    Int8Args a;
+    std::memset(&a, 0, sizeof(a));
+    a.theta = b->theta;
+    a.momentum = b->momentum;
+    for (int k = 0; k < b->k; ++k) a.replicas[k] = b->replicas[k];
+    a.n = b->n;
+    a.mu = static_cast<float>(co->mu);
+    a.eta = static_cast<float>(co->eta_out);
+    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    a.inv_k = 1.0 / static_cast<double>(b->k);
+    a.mean_codes = codes;
+    a.mean_scales = scales;
+    a.partials = c->partials;
+    a.ticket = c->ticket;
+    a.sums = c->sums;
+    const int rt = b->replica_dtype == AUTOLOCO_BF16 ? 1 : 0;
+    int per_cu = c->occupancy_int8[rt][b->k];
+    if (per_cu < 1) per_cu = 1;
+    int limit = c->grid_limit > 0 ? c->grid_limit : c->num_cus * per_cu;
+    if (limit > kMaxBlocks) limit = kMaxBlocks;
+    const int blocks = static_cast<int>(nblocks < limit ? nblocks : limit);
+    static const Int8Launcher table[2][2][2] = {
+        {{launch_int8_f32_s0r0, launch_int8_f32_s0r1}, {launch_int8_f32_s1r0, launch_int8_f32_s1r1}},
+        {{launch_int8_bf16_s0r0, launch_int8_bf16_s0r1}, {launch_int8_bf16_s1r0, launch_int8_bf16_s1r1}}};
+    hipError_t e;
+    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    e = table[rt][stats ? 1 : 0][reset ? 1 : 0](b->k, blocks, c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if (c->timing) {
+        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+        c->timed_valid = true;
+    }
+    if (stats) {
+        const size_t bytes = sizeof(double) * (2 * b->k + 1);
+        e = hipMemcpyAsync(c->host_sums, c->sums, bytes, hipMemcpyDeviceToHost, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync");
+        e = hipStreamSynchronize(c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        finish_stats(c->host_sums, b->k, eps, out);
+    }
+    c->err.clear();
+    return AUTOLOCO_OK;
 }
 
 int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {

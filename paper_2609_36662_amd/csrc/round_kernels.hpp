@@ -27,12 +27,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "reduce.hpp"
+
 namespace autoloco {
 
 constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / 64;
-constexpr int kMaxK = 16;
-constexpr int kMaxSums = 2 * kMaxK + 1;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -116,69 +115,6 @@ __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K]
         const float dir = __builtin_fmaf(a.mu, v_new, dt);
         th_new = __builtin_fmaf(-a.eta, dir, th);
     }
-}
-
-// --------------------------------------------------------------- reduction --
-// Sums acc[0..NS) over the workgroup; the result is valid in threads
-// 0..NS-1 (thread j holds sum j).  Fixed order throughout.
-template <int NS>
-__device__ __forceinline__ double block_reduce(double (&acc)[NS], double* lds) {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-        double v = acc[j];
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-        acc[j] = v;
-    }
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    if (lane == 0) {
-#pragma unroll
-        for (int j = 0; j < NS; ++j) lds[wave * NS + j] = acc[j];
-    }
-    __syncthreads();
-    double t = 0.0;
-    if (threadIdx.x < NS) {
-        t = lds[threadIdx.x];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) t += lds[w * NS + threadIdx.x];
-    }
-    __syncthreads();
-    return t;
-}
-
-// Stage 1 writes this workgroup's partials; the last workgroup to arrive
-// adds all partials in workgroup order and writes the final sums.
-template <int NS>
-__device__ __forceinline__ void grid_reduce(double (&acc)[NS], const RoundArgs& a) {
-    __shared__ double lds[kWaves * kMaxSums];
-    __shared__ int is_last;
-    const double part = block_reduce<NS>(acc, lds);
-    if (threadIdx.x < NS)
-        __hip_atomic_store(&a.partials[(int64_t)blockIdx.x * NS + threadIdx.x], part, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned int prev =
-            __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        is_last = (prev == gridDim.x - 1);
-    }
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();
-    double tot[NS];
-#pragma unroll
-    for (int j = 0; j < NS; ++j) tot[j] = 0.0;
-    for (unsigned int b = threadIdx.x; b < gridDim.x; b += kBlock) {
-#pragma unroll
-        for (int j = 0; j < NS; ++j)
-            tot[j] += __hip_atomic_load(&a.partials[(int64_t)b * NS + j], __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT);
-    }
-    const double fin = block_reduce<NS>(tot, lds);
-    if (threadIdx.x < NS) a.sums[threadIdx.x] = fin;
-    if (threadIdx.x == 0) __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ------------------------------------------------------------ round kernel --
@@ -328,7 +264,7 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
         }
     }
 
-    if constexpr (STATS) grid_reduce<NS>(acc, a);
+    if constexpr (STATS) grid_reduce<NS, kBlock>(acc, a.partials, a.ticket, a.sums);
 }
 
 // ------------------------------------------------------------ reset kernel --
