@@ -28,7 +28,7 @@ METRIC = "sync-round params/s and achieved HBM GB/s (% of peak), 1.1B params K=8
 PEAK_HBM_GBS = 8000.0
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_36662_amd", "csrc", f)
-                  for f in ("round_kernels.hpp", "round_inst.hip")]
+                  for f in ("round_kernels.hpp", "reduce.hpp", "round_inst.hip")]
 
 # name -> (shape, K, replica dtype, recipe, selected horizon, base horizon)
 WORKLOADS = {

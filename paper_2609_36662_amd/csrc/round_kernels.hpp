@@ -65,6 +65,21 @@ __device__ __forceinline__ void st_u4(void* p, u32x4 v) {
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// Same, at a wave-uniform base plus a 32-bit per-lane byte offset (lets the
+// compiler keep the base in scalar registers).
+__device__ __forceinline__ f32x4 ld_f4_at(const void* base, uint32_t off) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(static_cast<const char*>(base) + off));
+}
+__device__ __forceinline__ void st_f4_at(void* base, uint32_t off, f32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(static_cast<char*>(base) + off));
+}
+__device__ __forceinline__ u32x4 ld_u4_at(const void* base, uint32_t off) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const char*>(base) + off));
+}
+__device__ __forceinline__ void st_u4_at(void* base, uint32_t off, u32x4 v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(static_cast<char*>(base) + off));
+}
+
 // bf16 <-> fp32.  Widening is exact; narrowing rounds to nearest, ties to
 // even, keeps infinities and turns every NaN into the quiet NaN 0x7FC0 with
 // its sign.
@@ -130,15 +145,22 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
     const int64_t stride = (int64_t)gridDim.x * kBlock;
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
 
-    for (int64_t i = gtid; i < nvec; i += stride) {
-        const int64_t base = i * V;
+    // The loop walks wave-uniform windows of kBlock vectors: each stream's window
+    // base stays in scalar registers and a lane adds only its 32-bit offset.
+    for (int64_t vb = (int64_t)blockIdx.x * kBlock; vb < nvec; vb += stride) {
+        if (vb + threadIdx.x >= nvec) continue;
+        const int64_t wb = vb * V;                        // first parameter of the window
+        const uint32_t fo = threadIdx.x * (uint32_t)V * 4u; // this lane's byte offset in fp32 buffers
+        const uint32_t ro = threadIdx.x * 16u;             // and in replica buffers (16 bytes per lane)
+        float* const th_w = a.theta + wb;
+        float* const mo_w = UPDATE ? a.momentum + wb : nullptr;
         float th[V], v[V], r[K][V];
         if constexpr (RT == RT_F32) {
-            const f32x4 t4 = ld_f4(a.theta + base);
+            const f32x4 t4 = ld_f4_at(th_w, fo);
 #pragma unroll
             for (int e = 0; e < 4; ++e) th[e] = t4[e];
             if constexpr (UPDATE) {
-                const f32x4 v4 = ld_f4(a.momentum + base);
+                const f32x4 v4 = ld_f4_at(mo_w, fo);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = v4[e];
             } else {
@@ -147,19 +169,19 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                const f32x4 r4 = ld_f4(static_cast<const float*>(a.replicas[k]) + base);
+                const f32x4 r4 = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, ro);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
             }
         } else {
-            const f32x4 t0 = ld_f4(a.theta + base), t1 = ld_f4(a.theta + base + 4);
+            const f32x4 t0 = ld_f4_at(th_w, fo), t1 = ld_f4_at(th_w, fo + 16u);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 th[e] = t0[e];
                 th[4 + e] = t1[e];
             }
             if constexpr (UPDATE) {
-                const f32x4 v0 = ld_f4(a.momentum + base), v1 = ld_f4(a.momentum + base + 4);
+                const f32x4 v0 = ld_f4_at(mo_w, fo), v1 = ld_f4_at(mo_w, fo + 16u);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     v[e] = v0[e];
@@ -171,7 +193,7 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                const u32x4 w = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + base);
+                const u32x4 w = ld_u4_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, ro);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     r[k][2 * e] = bf16_lo(w[e]);
@@ -201,23 +223,23 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
         }
         if constexpr (UPDATE) {
             if constexpr (RT == RT_F32) {
-                st_f4(a.theta + base, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-                st_f4(a.momentum + base, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+                st_f4_at(th_w, fo, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+                st_f4_at(mo_w, fo, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
                 if constexpr (RESET) {
                     const f32x4 o = {th_new[0], th_new[1], th_new[2], th_new[3]};
 #pragma unroll
-                    for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + base, o);
+                    for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, ro, o);
                 }
             } else {
-                st_f4(a.theta + base, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-                st_f4(a.theta + base + 4, f32x4{th_new[4], th_new[5], th_new[6], th_new[7]});
-                st_f4(a.momentum + base, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
-                st_f4(a.momentum + base + 4, f32x4{v_new[4], v_new[5], v_new[6], v_new[7]});
+                st_f4_at(th_w, fo, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+                st_f4_at(th_w, fo + 16u, f32x4{th_new[4], th_new[5], th_new[6], th_new[7]});
+                st_f4_at(mo_w, fo, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+                st_f4_at(mo_w, fo + 16u, f32x4{v_new[4], v_new[5], v_new[6], v_new[7]});
                 if constexpr (RESET) {
                     const u32x4 o = {bf16_pack(th_new[0], th_new[1]), bf16_pack(th_new[2], th_new[3]),
                                      bf16_pack(th_new[4], th_new[5]), bf16_pack(th_new[6], th_new[7])};
 #pragma unroll
-                    for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + base, o);
+                    for (int k = 0; k < K; ++k) st_u4_at(static_cast<uint16_t*>(a.replicas[k]) + wb, ro, o);
                 }
             }
         }
