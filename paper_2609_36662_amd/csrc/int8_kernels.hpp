@@ -213,7 +213,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                     uint32_t w = 0;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) w |= (uint32_t)(uint8_t)(int8_t)qm[4 * g + e] << (8 * e);
-                    *reinterpret_cast<uint32_t*>(a.mean_codes + off[g]) = w;
+                    __builtin_nontemporal_store(w, reinterpret_cast<uint32_t*>(a.mean_codes + off[g]));
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)

@@ -245,3 +245,12 @@ def test_controller_checkpoint_resume_is_bitwise():
     bad[0] ^= 0xFF
     with pytest.raises(al.AutolocoError):
         al.autoloco_controller_load(resumed, bytes(bad))
+
+
+def test_device_calls_fail_loudly_without_a_gpu():
+    # no silent CPU path: without a visible GPU a context cannot be created
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is visible")
+    with pytest.raises(RuntimeError):
+        al.autoloco_create(0)
