@@ -13,7 +13,8 @@
 //   Q_k += (Delta_k - Delta_agg)^2, M += Delta_agg^2          C uses the aggregate
 //   corrected Nesterov step with Delta_agg, reset of the replicas
 // The two block maxima (the K worker maxima, then the mean's) are exact and
-// order-independent: a wavefront butterfly of fmaxf and the waves through LDS.
+// order-independent: a wavefront max over DPP lane exchanges, then the waves
+// through LDS, with one barrier each.
 // Every codec step runs in fp32 with IEEE division and round-to-nearest-even,
 // so the codes are the same integers the FP32 definition gives.
 #pragma once
@@ -48,53 +49,71 @@ __device__ __forceinline__ float codec_scale(float amax) {
     return s < 0x1p-126f ? 0x1p-126f : s;
 }
 
-__device__ __forceinline__ float codec_q(float x, float s) {
-    float q = __builtin_rintf(x / s);
+// Code of x at scale s (r = fp32(1/s)): the integer nearest fp32(x / s), ties
+// to even, clipped to +-127.  t = x * r differs from fp32(x / s) by at most
+// 1.5 * 2^-23 * |x / s| <= 2.3e-5 here (|x / s| <= 127), so rint(t) is the
+// same integer unless t lies within that distance of a half-integer; only
+// then (about 1e-4 of the elements) is the IEEE quotient formed.
+__device__ __forceinline__ float codec_q(float x, float s, float r) {
+    const float t = x * r;
+    float q = __builtin_rintf(t);
+    if (!(0.5f - fabsf(t - q) > 6.0e-5f)) q = __builtin_rintf(x / s);
     q = q < -127.0f ? -127.0f : q;
     return q > 127.0f ? 127.0f : q;
 }
 
-// Maximum of NV values over the workgroup (every thread gets the result).
+// Maximum over the 64 lanes of a wavefront of a non-negative float (or NaN),
+// compared as its bit pattern, which orders non-negative floats as numbers:
+// DPP exchanges within each row of 16 lanes, then the four row results are read
+// out as wave-uniform values.
+__device__ __forceinline__ uint32_t wave_max_bits(uint32_t x) {
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));  // row_mirror
+    const uint32_t a = max((uint32_t)__builtin_amdgcn_readlane((int)x, 0), (uint32_t)__builtin_amdgcn_readlane((int)x, 16));
+    const uint32_t b = max((uint32_t)__builtin_amdgcn_readlane((int)x, 32), (uint32_t)__builtin_amdgcn_readlane((int)x, 48));
+    return max(a, b);
+}
+
+// Maximum of NV non-negative values over the workgroup (every thread gets the
+// result).  One barrier: the caller gives each use within a loop iteration its
+// own LDS region, so a wave that runs ahead into the next iteration writes a
+// region every other wave has finished reading (they all passed a later
+// barrier of this iteration after reading it).  Every thread of the workgroup
+// must be active.
 template <int NV, int NT>
-__device__ __forceinline__ void block_max(float (&v)[NV], float* lds) {
+__device__ __forceinline__ void block_max(float (&v)[NV], uint32_t* lds) {
     constexpr int NW = NT / 64;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        float x = v[j];
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
-        v[j] = x;
-    }
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    if (lane == 0) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j) lds[wave * NV + j] = v[j];
+    for (int j = 0; j < NV; ++j) {
+        const uint32_t m = wave_max_bits(__float_as_uint(v[j]));
+        if (lane == 0) lds[j * NW + wave] = m;
     }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
-        float x = lds[j];
+        uint32_t x = lds[j * NW];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) x = fmaxf(x, lds[w * NV + j]);
-        v[j] = x;
+        for (int w = 1; w < NW; ++w) x = max(x, lds[j * NW + w]);
+        v[j] = __uint_as_float(x);
     }
-    __syncthreads();
 }
 
 constexpr int kInt8Threads = 512;  // one codec block of 4,096 parameters per workgroup
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Thread t of a workgroup owns parameters blk*4096 + g*2048 + 4t + e for
-// g in {0,1}, e in 0..3: every load and store instruction of a wavefront
-// covers one contiguous 1 KB (fp32) or 512 B (bf16) run.
+// Each thread of a workgroup owns 8 parameters of the block (see the loop).
 template <int K, int RT, bool STATS, bool RESET>
 __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr int NT = kInt8Threads;
     constexpr int V = 8;
     constexpr int NS = STATS ? 2 * K + 1 : 1;
-    __shared__ float lds_max[kMaxWaves * kMaxK];
+    __shared__ uint32_t lds_max[NT / 64 * K];   // worker block maxima
+    __shared__ uint32_t lds_mmax[NT / 64];      // the mean's block maximum
 
     double acc[NS];
 #pragma unroll
@@ -102,47 +121,59 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 
     const int64_t nblocks = (a.n + kCodecBlock - 1) / kCodecBlock;
     for (int64_t blk = blockIdx.x; blk < nblocks; blk += gridDim.x) {
-        int64_t off[2];
-        int valid[2];
+        // fp32 replicas: two runs of 4 parameters, 2,048 apart (each wavefront
+        // instruction covers 1 KB); bf16 replicas: one run of 8 parameters (16 B
+        // of each replica per lane, as the plain round loads them)
+        constexpr int G = RT == RT_F32 ? 2 : 1;
+        constexpr int W = V / G;
+        int64_t off[G];
+        int valid[G];
+        bool ok[V];
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            off[g] = blk * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * 4;
+        for (int g = 0; g < G; ++g) {
+            off[g] = blk * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W;
             const int64_t left = a.n - off[g];
-            valid[g] = left >= 4 ? 4 : (left > 0 ? (int)left : 0);
+            valid[g] = left >= W ? W : (left > 0 ? (int)left : 0);
+#pragma unroll
+            for (int e = 0; e < W; ++e) ok[g * W + e] = e < valid[g];
         }
 
         float th[V], v[V], d[K][V];
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
+        for (int g = 0; g < G; ++g) {
             const int64_t o = off[g];
-            if (valid[g] == 4) {
-                const f32x4 t4 = ld_f4(a.theta + o), v4 = ld_f4(a.momentum + o);
+            if (valid[g] == W) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    th[4 * g + e] = t4[e];
-                    v[4 * g + e] = v4[e];
+                for (int h = 0; h < W / 4; ++h) {
+                    const f32x4 t4 = ld_f4(a.theta + o + 4 * h), v4 = ld_f4(a.momentum + o + 4 * h);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        th[g * W + 4 * h + e] = t4[e];
+                        v[g * W + 4 * h + e] = v4[e];
+                    }
                 }
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                     if constexpr (RT == RT_F32) {
                         const f32x4 r4 = ld_f4(static_cast<const float*>(a.replicas[k]) + o);
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) d[k][4 * g + e] = th[4 * g + e] - r4[e];
+                        for (int e = 0; e < 4; ++e) d[k][g * W + e] = th[g * W + e] - r4[e];
                     } else {
-                        const u32x2 w = __builtin_nontemporal_load(
-                            reinterpret_cast<const u32x2*>(static_cast<const uint16_t*>(a.replicas[k]) + o));
-                        d[k][4 * g + 0] = th[4 * g + 0] - bf16_lo(w[0]);
-                        d[k][4 * g + 1] = th[4 * g + 1] - bf16_hi(w[0]);
-                        d[k][4 * g + 2] = th[4 * g + 2] - bf16_lo(w[1]);
-                        d[k][4 * g + 3] = th[4 * g + 3] - bf16_hi(w[1]);
+                        const u32x4 w = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + o);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            d[k][2 * e] = th[2 * e] - bf16_lo(w[e]);
+                            d[k][2 * e + 1] = th[2 * e + 1] - bf16_hi(w[e]);
+                        }
                     }
                 }
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
+                for (int e = 0; e < W; ++e) {
                     const bool in = e < valid[g];
-                    th[4 * g + e] = in ? a.theta[o + e] : 0.0f;
-                    v[4 * g + e] = in ? a.momentum[o + e] : 0.0f;
+                    const int x = g * W + e;
+                    th[x] = in ? a.theta[o + e] : 0.0f;
+                    v[x] = in ? a.momentum[o + e] : 0.0f;
 #pragma unroll
                     for (int k = 0; k < K; ++k) {
                         float r = 0.0f;
@@ -152,7 +183,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                             else
                                 r = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.replicas[k])[o + e] << 16);
                         }
-                        d[k][4 * g + e] = in ? th[4 * g + e] - r : 0.0f;
+                        d[k][x] = in ? th[x] - r : 0.0f;
                     }
                 }
             }
@@ -187,8 +218,9 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
         for (int k = 0; k < K; ++k) {
             const float s = codec_scale(amax[k]);
+            const float r = 1.0f / s;
 #pragma unroll
-            for (int e = 0; e < V; ++e) sum[e] += (double)(codec_q(d[k][e], s) * s);
+            for (int e = 0; e < V; ++e) sum[e] += (double)(codec_q(d[k][e], s, r) * s);
         }
         float mean[V];
         float mmax[1] = {0.f};
@@ -197,27 +229,35 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             mean[e] = (float)(sum[e] * a.inv_k);
             mmax[0] = fmaxf(mmax[0], fabsf(mean[e]));
         }
-        block_max<1, NT>(mmax, lds_max);
+        block_max<1, NT>(mmax, lds_mmax);
         const float sm = codec_scale(mmax[0]);
+        const float rm = 1.0f / sm;
 
         float agg[V], qm[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            qm[e] = codec_q(mean[e], sm);
-            agg[e] = e % 4 < valid[e / 4] ? qm[e] * sm : 0.0f;
+            qm[e] = codec_q(mean[e], sm, rm);
+            agg[e] = ok[e] ? qm[e] * sm : 0.0f;
         }
         if (a.mean_codes != nullptr) {
 #pragma unroll
-            for (int g = 0; g < 2; ++g) {
-                if (valid[g] == 4) {
-                    uint32_t w = 0;
+            for (int g = 0; g < G; ++g) {
+                if (valid[g] == W) {
+                    uint32_t w[W / 4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) w |= (uint32_t)(uint8_t)(int8_t)qm[4 * g + e] << (8 * e);
-                    __builtin_nontemporal_store(w, reinterpret_cast<uint32_t*>(a.mean_codes + off[g]));
+                    for (int h = 0; h < W / 4; ++h) {
+                        w[h] = 0;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) w[h] |= (uint32_t)(uint8_t)(int8_t)qm[g * W + 4 * h + e] << (8 * e);
+                    }
+                    if constexpr (W == 4)
+                        __builtin_nontemporal_store(w[0], reinterpret_cast<uint32_t*>(a.mean_codes + off[g]));
+                    else
+                        __builtin_nontemporal_store(u32x2{w[0], w[1]}, reinterpret_cast<u32x2*>(a.mean_codes + off[g]));
                 } else {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (e < valid[g]) a.mean_codes[off[g] + e] = (int8_t)qm[4 * g + e];
+                    for (int e = 0; e < W; ++e)
+                        if (e < valid[g]) a.mean_codes[off[g] + e] = (int8_t)qm[g * W + e];
                 }
             }
             if (threadIdx.x == 0) a.mean_scales[blk] = sm;
@@ -250,28 +290,31 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             th_new[e] = __builtin_fmaf(-a.eta, dir, th[e]);
         }
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
+        for (int g = 0; g < G; ++g) {
             const int64_t o = off[g];
-            const float* tn = th_new + 4 * g;
-            const float* vn = v_new + 4 * g;
-            if (valid[g] == 4) {
-                st_f4(a.theta + o, f32x4{tn[0], tn[1], tn[2], tn[3]});
-                st_f4(a.momentum + o, f32x4{vn[0], vn[1], vn[2], vn[3]});
+            const float* tn = th_new + g * W;
+            const float* vn = v_new + g * W;
+            if (valid[g] == W) {
+#pragma unroll
+                for (int h = 0; h < W / 4; ++h) {
+                    st_f4(a.theta + o + 4 * h, f32x4{tn[4 * h], tn[4 * h + 1], tn[4 * h + 2], tn[4 * h + 3]});
+                    st_f4(a.momentum + o + 4 * h, f32x4{vn[4 * h], vn[4 * h + 1], vn[4 * h + 2], vn[4 * h + 3]});
+                }
                 if constexpr (RESET) {
                     if constexpr (RT == RT_F32) {
                         const f32x4 t4 = {tn[0], tn[1], tn[2], tn[3]};
 #pragma unroll
                         for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + o, t4);
                     } else {
-                        const u32x2 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3])};
+                        const u32x4 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3]), bf16_pack(tn[4], tn[5]),
+                                         bf16_pack(tn[6], tn[7])};
 #pragma unroll
-                        for (int k = 0; k < K; ++k)
-                            __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.replicas[k]) + o));
+                        for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + o, w);
                     }
                 }
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
+                for (int e = 0; e < W; ++e) {
                     if (e < valid[g]) {
                         a.theta[o + e] = tn[e];
                         a.momentum[o + e] = vn[e];
