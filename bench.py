@@ -72,26 +72,62 @@ def committed_traffic(tag: str):
         return None
 
 
-def cpu_baseline(sample, coeffs, seconds: float, desc: str):
-    """The float64 oracle, as it stands, on a bounded sample of the workload."""
+def cpu_baseline(sample, coeffs, seconds: float, desc: str, threads: int = 1):
+    """The float64 oracle, as it stands, on a bounded sample of the workload.
+
+    The sample is cut into 16 fixed chunks that run through the oracle one
+    after another, or with ``threads`` > 1 on a pool of threads (numpy releases
+    the interpreter lock inside its array operations); the chunks' sums are
+    combined in chunk order."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import round as orr
     th, mom, reps, rdt = sample
     n = th.shape[0]
-    done = 0
-    t0 = time.perf_counter()
-    while True:
-        res = orr.sync_round(th, mom, reps, coeffs.mu, coeffs.eta_out, coeffs.rho, bool(coeffs.normalize),
-                             1e-12)
-        orr.reset_replicas(res.theta, len(reps), rdt)
-        done += n
-        if time.perf_counter() - t0 >= seconds:
-            break
-    dt = time.perf_counter() - t0
+    k = len(reps)
+    step = -(-n // 16)
+    bounds = [(lo, min(n, lo + step)) for lo in range(0, n, step)]
+
+    def chunk(lo_hi):
+        lo, hi = lo_hi
+        res = orr.sync_round(th[lo:hi], mom[lo:hi], [r[lo:hi] for r in reps], coeffs.mu, coeffs.eta_out,
+                             coeffs.rho, bool(coeffs.normalize), 1e-12)
+        orr.reset_replicas(res.theta, k, rdt)
+        return res.stats
+
+    def one_round(pool):
+        parts = list(pool.map(chunk, bounds)) if pool is not None else [chunk(b) for b in bounds]
+        s = [sum(p.sq_norm[i] for p in parts) for i in range(k)]
+        q = [sum(p.sq_dev[i] for p in parts) for i in range(k)]
+        return orr.finish_stats(s, q, sum(p.sq_mean for p in parts), 1e-12)
+
+    pool = ThreadPoolExecutor(threads) if threads > 1 else None
+    try:
+        done = 0
+        t0 = time.perf_counter()
+        while True:
+            one_round(pool)
+            done += n
+            if time.perf_counter() - t0 >= seconds:
+                break
+        dt = time.perf_counter() - t0
+    finally:
+        if pool is not None:
+            pool.shutdown()
     del np
-    return {"value": done / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
+    how = "16 chunks on one thread" if threads == 1 else f"16 chunks on {threads} threads"
+    return {"value": done / dt, "unit": "params/s", "cores": threads, "kind": "oracle",
             "sample": f"{desc}: first {n:,} parameters of every buffer, round repeated "
-                      f"{done // n}x over {dt:.1f} s (numpy float64, one thread)"}
+                      f"{done // n}x over {dt:.1f} s (numpy float64, {how})"}
+
+
+def host_threads() -> int:
+    """Host cores this process may use, capped at a one-GPU share of 16."""
+    try:
+        p = len(os.sched_getaffinity(0))
+    except AttributeError:
+        p = os.cpu_count() or 1
+    return max(1, min(16, p))
 
 
 def main() -> int:
@@ -236,10 +272,13 @@ def main() -> int:
     tag = f"round_{rdt}_k{k}_{args.workload}" + ("_int8" if args.codec == "int8" else "")
     traffic = committed_traffic(tag)
 
-    cpu = None
+    cpu = cpu1 = None
     if sample is not None:
-        log("timing the oracle on the CPU sample")
-        cpu = cpu_baseline(sample, coeffs, args.cpu_seconds, f"{args.workload} K={k} {rdt}")
+        desc = f"{args.workload} K={k} {rdt}"
+        p = host_threads()
+        log(f"timing the oracle on the CPU sample: one thread, then {p} threads")
+        cpu1 = cpu_baseline(sample, coeffs, args.cpu_seconds, desc)
+        cpu = cpu_baseline(sample, coeffs, args.cpu_seconds, desc, threads=p) if p > 1 else cpu1
 
     out = {
         "metric": METRIC,
@@ -275,6 +314,7 @@ def main() -> int:
         "first_round_stats": {k2: first_stats[k2] for k2 in ("D", "C", "disagreement", "finite")}
         if first_stats else None,
         "cpu_baseline": cpu,
+        "cpu_baseline_one_thread": cpu1,
         "kernel_source_sha256_16": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
