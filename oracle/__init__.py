@@ -25,6 +25,10 @@ Modules
                 App. B.2-B.4).
   controller  — the adaptive interval controller and token mapper (Sec.
                 "Adaptive Interval Selection"; App. A).
+  int8_codec  — the INT8 blockwise pseudo-gradient codec and the round that
+                averages through it (App. G.1).
+  adamw       — one inner AdamW step of every worker with its own
+                gradient-norm clipping (Table "Training settings"; App. G.1).
 
 Parity unpinned (no value printed by the paper and no closed form fixes them;
 each is one reading of a point the paper leaves open):
