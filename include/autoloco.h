@@ -206,6 +206,66 @@ int autoloco_outer_step_int8(autoloco_ctx* ctx, const autoloco_buffers* bufs,
 int autoloco_broadcast_reset(autoloco_ctx* ctx, const autoloco_buffers* bufs);
 
 /* ------------------------------------------------------------------------ */
+/* Inner AdamW step of the K workers                                         */
+/* ------------------------------------------------------------------------ */
+
+/* Each worker's state for its local inner loop (Alg. "AutoLoCo outer
+ * interval", local inner loops; App. G.1 keeps master parameters and AdamW
+ * states in FP32 and computes the model in BF16).  All buffers are device
+ * memory owned by the caller, [n] elements, 16-byte aligned, pairwise
+ * disjoint.  params, exp_avg and exp_avg_sq are read and written; grads are
+ * read; model_bf16 (bf16 bit patterns) is written iff set: set all k of them
+ * or none. */
+typedef struct {
+    int64_t n;
+    int32_t k;
+    float* params[AUTOLOCO_MAX_K];       /* worker k's FP32 master parameters */
+    float* exp_avg[AUTOLOCO_MAX_K];      /* first moment m */
+    float* exp_avg_sq[AUTOLOCO_MAX_K];   /* second moment v */
+    const float* grads[AUTOLOCO_MAX_K];  /* this step's gradient of worker k */
+    void* model_bf16[AUTOLOCO_MAX_K];    /* BF16 compute copy of the new params, or NULL */
+} autoloco_adamw_buffers;
+
+/* Settings of one step, shared by all workers (Table "Training settings":
+ * C4 uses beta = (0.9, 0.95), weight decay 0.1, clipping 1.0; SFT
+ * (0.9, 0.999), 0, 1.0).  lr is the schedule's value at this step
+ * (autoloco_inner_lr); step counts from 1 and sets the bias corrections;
+ * max_grad_norm = 0 turns clipping off. */
+typedef struct {
+    double lr, beta1, beta2, eps, weight_decay, max_grad_norm;
+    int64_t step;
+} autoloco_adamw_coeffs;
+
+/* Per-worker gradient norms of the step and the clipping factors applied. */
+typedef struct {
+    double grad_norm[AUTOLOCO_MAX_K];
+    double clip_coef[AUTOLOCO_MAX_K];
+    int32_t k;
+    int32_t finite;   /* every gradient norm is finite */
+} autoloco_adamw_stats;
+
+/* One AdamW step of every worker, each clipped by its own global gradient
+ * norm: c_k = min(1, max_grad_norm / (||g_k|| + 1e-6)), g <- c_k g, then
+ * decoupled weight decay theta <- theta (1 - lr wd), m <- beta1 m +
+ * (1 - beta1) g, v <- beta2 v + (1 - beta2) g^2 and theta <- theta - lr
+ * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps).  With clipping (or
+ * out) a first pass sums each worker's g^2 (fp64, deterministic order); the
+ * update pass reads those sums on the device.  With out the call blocks until
+ * the norms are on the host; without, it is asynchronous on the stream.
+ * Element arithmetic is fp32 with the step's scalars rounded once to fp32.
+ * A non-finite gradient is not an error: it propagates into the state and
+ * finite = 0.
+ * Errors: E_INVALID (k outside 1..16, n < 0, null buffer, partial model_bf16,
+ * step < 1, lr / eps / weight_decay / max_grad_norm negative or not finite,
+ * beta outside [0, 1)), E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_inner_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* bufs,
+                         const autoloco_adamw_coeffs* coeffs, autoloco_adamw_stats* out);
+
+/* Device milliseconds of the two passes of the last timed autoloco_inner_adamw
+ * call (norm_ms = 0 if the norm pass did not run); waits for them to finish. */
+int autoloco_last_adamw_ms(autoloco_ctx* ctx, float* norm_ms, float* update_ms);
+
+/* ------------------------------------------------------------------------ */
 /* Host-only scalar routines                                                 */
 /* ------------------------------------------------------------------------ */
 

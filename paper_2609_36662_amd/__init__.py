@@ -1,7 +1,8 @@
 """AutoLoCo synchronisation round on AMD Instinct MI355X (gfx950).
 
 The round (pseudo-gradients, their mean, the D/C diagnostics, the corrected
-Nesterov outer step and the replica reset) runs in hand-written HIP kernels
+Nesterov outer step and the replica reset), and the workers' inner AdamW
+step between rounds, run in hand-written HIP kernels
 behind the C ABI of include/autoloco.h; the interval controller and the outer
 correction are host C++ behind the same ABI.  This package is the thin Python
 binding (same names as the C calls) and the in-tree build.
@@ -14,4 +15,5 @@ from ._lib import (  # noqa: F401
     autoloco_lr_mass, autoloco_outer_correction, autoloco_outer_step, autoloco_outer_step_int8, autoloco_round_stats,
     autoloco_select_interval, autoloco_set_grid_limit, autoloco_set_timing, default_controller_cfg,
     lib, make_buffers, make_coeffs, make_observation, make_outer_cfg, make_schedule, spread_tensors,
+    autoloco_inner_adamw, autoloco_last_adamw_ms, make_adamw_buffers, make_adamw_coeffs,
 )

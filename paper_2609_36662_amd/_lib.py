@@ -94,6 +94,22 @@ class Decision(C.Structure):
                 ("done", C.c_int32), ("reserved", C.c_int32), ("coeffs", OuterCoeffs)]
 
 
+class AdamWBuffers(C.Structure):
+    _fields_ = [("n", C.c_int64), ("k", C.c_int32), ("params", C.c_void_p * MAX_K),
+                ("exp_avg", C.c_void_p * MAX_K), ("exp_avg_sq", C.c_void_p * MAX_K),
+                ("grads", C.c_void_p * MAX_K), ("model_bf16", C.c_void_p * MAX_K)]
+
+
+class AdamWCoeffs(C.Structure):
+    _fields_ = [("lr", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
+                ("weight_decay", C.c_double), ("max_grad_norm", C.c_double), ("step", C.c_int64)]
+
+
+class AdamWStats(C.Structure):
+    _fields_ = [("grad_norm", C.c_double * MAX_K), ("clip_coef", C.c_double * MAX_K),
+                ("k", C.c_int32), ("finite", C.c_int32)]
+
+
 # ---------------------------------------------------------------- loading --
 _lib = None
 _lock = threading.Lock()
@@ -118,6 +134,9 @@ SYMBOLS = [
     ("autoloco_outer_step_int8", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p, C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
+    ("autoloco_inner_adamw", C.c_int, [C.c_void_p, C.POINTER(AdamWBuffers), C.POINTER(AdamWCoeffs),
+                                       C.POINTER(AdamWStats)]),
+    ("autoloco_last_adamw_ms", C.c_int, [C.c_void_p, C.POINTER(C.c_float), C.POINTER(C.c_float)]),
     ("autoloco_inner_lr", C.c_double, [C.POINTER(Schedule), C.c_int64]),
     ("autoloco_lr_mass", C.c_double, [C.POINTER(Schedule), C.c_int64, C.c_int64]),
     ("autoloco_outer_correction", C.c_int, [C.POINTER(OuterCfg), C.c_double, C.c_double,
@@ -389,6 +408,66 @@ def autoloco_broadcast_reset(ctx: Context, theta, replicas, n=None) -> None:
 
 
 # -------------------------------------------------------- host scalars --
+def make_adamw_coeffs(lr: float, step: int, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1,
+                      max_grad_norm=1.0) -> AdamWCoeffs:
+    """Settings of one inner step (defaults: the C4 recipe)."""
+    return AdamWCoeffs(float(lr), float(beta1), float(beta2), float(eps), float(weight_decay),
+                       float(max_grad_norm), int(step))
+
+
+def make_adamw_buffers(params: Sequence, exp_avg: Sequence, exp_avg_sq: Sequence, grads: Sequence,
+                       model_bf16: Optional[Sequence] = None, n: Optional[int] = None) -> AdamWBuffers:
+    """Describe the workers' caller-owned device tensors to the library (no copies)."""
+    import torch
+    k = len(params)
+    if not 1 <= k <= MAX_K:
+        raise ValueError(f"need 1..{MAX_K} workers, got {k}")
+    groups = [list(params), list(exp_avg), list(exp_avg_sq), list(grads)]
+    if any(len(g) != k for g in groups) or (model_bf16 is not None and len(model_bf16) != k):
+        raise ValueError("every per-worker list needs one tensor per worker")
+    count = params[0].numel() if n is None else int(n)
+    for g in groups:
+        for t in g:
+            if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or not t.is_contiguous():
+                raise TypeError("all buffers must be contiguous CUDA (HIP) tensors")
+            if t.dtype != torch.float32:
+                raise TypeError("params, moments and gradients must be float32")
+            if t.numel() < count:
+                raise ValueError("a buffer is shorter than n")
+    b = AdamWBuffers()
+    b.n = count
+    b.k = k
+    for i in range(k):
+        b.params[i] = params[i].data_ptr()
+        b.exp_avg[i] = exp_avg[i].data_ptr()
+        b.exp_avg_sq[i] = exp_avg_sq[i].data_ptr()
+        b.grads[i] = grads[i].data_ptr()
+        if model_bf16 is not None:
+            t = model_bf16[i]
+            if t.dtype != torch.bfloat16 or not t.is_contiguous() or t.numel() < count:
+                raise TypeError("model_bf16 must be contiguous bfloat16 tensors of at least n elements")
+            b.model_bf16[i] = t.data_ptr()
+    return b
+
+
+def autoloco_inner_adamw(ctx: Context, params, exp_avg, exp_avg_sq, grads, coeffs: AdamWCoeffs,
+                         model_bf16=None, stats: bool = True, n=None) -> Optional[AdamWStats]:
+    """One AdamW step of every worker; returns the gradient norms (stats=True)
+    or None (asynchronous on the context's stream)."""
+    b = make_adamw_buffers(params, exp_avg, exp_avg_sq, grads, model_bf16, n)
+    out = AdamWStats() if stats else None
+    _check(lib().autoloco_inner_adamw(ctx.handle, C.byref(b), C.byref(coeffs),
+                                      C.byref(out) if out is not None else None), "autoloco_inner_adamw", ctx)
+    return out
+
+
+def autoloco_last_adamw_ms(ctx: Context):
+    """(norm pass ms, update pass ms) of the last timed AdamW step."""
+    a, b = C.c_float(), C.c_float()
+    _check(lib().autoloco_last_adamw_ms(ctx.handle, C.byref(a), C.byref(b)), "autoloco_last_adamw_ms", ctx)
+    return a.value, b.value
+
+
 def make_schedule(peak=4e-4, min_lr=0.0, warmup=1000, total=50_000) -> Schedule:
     s = Schedule()
     s.peak, s.min_lr, s.warmup, s.total = peak, min_lr, warmup, total

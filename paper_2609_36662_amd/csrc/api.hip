@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "autoloco.h"
+#include "adamw_kernels.hpp"
 #include "int8_kernels.hpp"
 #include "round_kernels.hpp"
 
@@ -35,7 +36,9 @@ struct autoloco_ctx {
     double* host_sums = nullptr;
     bool timing = false;
     bool timed_valid = false;
-    hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+    hipEvent_t ev_start = nullptr, ev_stop = nullptr, ev_mid = nullptr;
+    bool adamw_timed = false;     // the last timed call was an AdamW step
+    bool adamw_norm_ran = false;  // ... and it ran the norm pass (ev_start..ev_mid)
     std::string err;
 };
 
@@ -85,6 +88,17 @@ int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k) {
     int64_t want = (nvec + kBlock - 1) / kBlock;
     if (want < 1) want = 1;
     return static_cast<int>(want < limit ? want : limit);
+}
+
+// Workgroups per worker of the AdamW update: about three per compute unit in
+// total, split evenly over the workers' grid rows.
+int adamw_blocks(const autoloco_ctx* ctx, int64_t n, int k) {
+    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * 3;
+    if (limit > kMaxBlocks) limit = kMaxBlocks;
+    int per = (limit + k - 1) / k;
+    const int64_t want = (n / 4 + kBlock - 1) / kBlock;
+    if (want < per) per = static_cast<int>(want);
+    return per < 1 ? 1 : per;
 }
 
 struct Range {
@@ -186,6 +200,7 @@ int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, 
     if (ctx->timing) {
         if ((e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
         ctx->timed_valid = true;
+        ctx->adamw_timed = false;
     }
     if (stats) {
         const size_t bytes = sizeof(double) * (2 * b->k + 1);
@@ -197,6 +212,57 @@ int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, 
     }
     ctx->err.clear();
     return AUTOLOCO_OK;
+}
+
+
+// Checks the AdamW buffers: sizes, pointers, alignment and overlap.
+int validate_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* b, bool* copy) {
+    if (ctx == nullptr) return AUTOLOCO_E_INVALID;
+    if (b == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null buffers");
+    if (b->n < 0) return fail(ctx, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(ctx, AUTOLOCO_E_INVALID, "k outside 1..16");
+    int ncopy = 0;
+    for (int k = 0; k < b->k; ++k) ncopy += b->model_bf16[k] != nullptr;
+    if (ncopy != 0 && ncopy != b->k) return fail(ctx, AUTOLOCO_E_INVALID, "model_bf16 set for some workers only");
+    *copy = ncopy != 0;
+    if (b->n == 0) return AUTOLOCO_OK;
+    std::vector<Range> r;
+    const uintptr_t fbytes = static_cast<uintptr_t>(b->n) * 4u;
+    for (int k = 0; k < b->k; ++k) {
+        const void* ptrs[5] = {b->params[k], b->exp_avg[k], b->exp_avg_sq[k], b->grads[k], b->model_bf16[k]};
+        static const char* names[5] = {"params", "exp_avg", "exp_avg_sq", "grads", "model_bf16"};
+        for (int j = 0; j < 5; ++j) {
+            if (j == 4 && !*copy) continue;
+            if (ptrs[j] == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, std::string("null ") + names[j]);
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(ptrs[j]);
+            r.push_back({lo, lo + (j == 4 ? fbytes / 2 : fbytes), names[j]});
+        }
+    }
+    for (const Range& x : r)
+        if (x.lo % 16 != 0) return fail(ctx, AUTOLOCO_E_ALIGN, std::string(x.name) + " not 16-byte aligned");
+    for (size_t i = 0; i < r.size(); ++i)
+        for (size_t j = i + 1; j < r.size(); ++j)
+            if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
+                return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    return AUTOLOCO_OK;
+}
+
+double adamw_clip(double norm_sq, double max_norm) {
+    if (max_norm == 0.0) return 1.0;
+    const double c = max_norm / (std::sqrt(norm_sq) + 1e-6);
+    return c > 1.0 ? 1.0 : c;
+}
+
+void finish_adamw(const double* sums, int k, double max_norm, autoloco_adamw_stats* out) {
+    std::memset(out, 0, sizeof(*out));
+    out->k = k;
+    bool fin = true;
+    for (int i = 0; i < k; ++i) {
+        out->grad_norm[i] = std::sqrt(sums[i]);
+        out->clip_coef[i] = adamw_clip(sums[i], max_norm);
+        fin = fin && std::isfinite(out->grad_norm[i]);
+    }
+    out->finite = fin ? 1 : 0;
 }
 
 void zero_stats(int k, double eps, autoloco_stats* out) {
@@ -235,7 +301,8 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
               hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
               hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocDefault) == hipSuccess;
     ok = ok && hipMemset(c->ticket, 0, 256) == hipSuccess && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
-    ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess;
+    ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess &&
+         hipEventCreate(&c->ev_mid) == hipSuccess;
     ok = ok && hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         autoloco_destroy(c);
@@ -256,6 +323,7 @@ void autoloco_destroy(autoloco_ctx* c) {
         if (c->host_sums) (void)hipHostFree(c->host_sums);
         if (c->ev_start) (void)hipEventDestroy(c->ev_start);
         if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
+        if (c->ev_mid) (void)hipEventDestroy(c->ev_mid);
     }
     delete c;
 }
@@ -411,6 +479,7 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
     if (c->timing) {
         if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
         c->timed_valid = true;
+        c->adamw_timed = false;
     }
     if (stats) {
         const size_t bytes = sizeof(double) * (2 * b->k + 1);
@@ -439,6 +508,7 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
     if (c->timing) {
         if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
         c->timed_valid = true;
+        c->adamw_timed = false;
     }
     c->err.clear();
     return AUTOLOCO_OK;
@@ -503,6 +573,98 @@ int autoloco_free(autoloco_ctx* c, void* ptr) {
     DeviceGuard g(c->device);
     const hipError_t e = hipFree(ptr);
     if (e != hipSuccess) return hip_fail(c, e, "hipFree");
+    return AUTOLOCO_OK;
+}
+
+int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const autoloco_adamw_coeffs* co,
+                         autoloco_adamw_stats* out) {
+    bool copy = false;
+    int st = validate_adamw(c, b, &copy);
+    if (st != AUTOLOCO_OK) return st;
+    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
+    if (co->step < 1) return fail(c, AUTOLOCO_E_INVALID, "step counts from 1");
+    const double nonneg[4] = {co->lr, co->eps, co->weight_decay, co->max_grad_norm};
+    for (double x : nonneg)
+        if (!(std::isfinite(x) && x >= 0.0))
+            return fail(c, AUTOLOCO_E_INVALID, "lr, eps, weight_decay and max_grad_norm must be finite and >= 0");
+    if (!(co->beta1 >= 0.0 && co->beta1 < 1.0 && co->beta2 >= 0.0 && co->beta2 < 1.0))
+        return fail(c, AUTOLOCO_E_INVALID, "betas must lie in [0, 1)");
+    const bool clip = co->max_grad_norm > 0.0;
+    if (b->n == 0) {
+        if (out != nullptr) {
+            double z[AUTOLOCO_MAX_K] = {0};
+            finish_adamw(z, b->k, co->max_grad_norm, out);
+        }
+        return AUTOLOCO_OK;
+    }
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    const bool norm_pass = clip || out != nullptr;
+    hipError_t e;
+    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    if (norm_pass) {
+        GradNormArgs na;
+        std::memset(&na, 0, sizeof(na));
+        for (int k = 0; k < b->k; ++k) na.grads[k] = b->grads[k];
+        na.n = b->n;
+        na.partials = c->partials;
+        na.ticket = c->ticket;
+        na.sums = c->sums;
+        e = launch_grad_norm(b->k, blocks_for(c, b->n, AUTOLOCO_F32, b->k), c->stream, na);
+        if (e != hipSuccess) return hip_fail(c, e, "gradient norm launch");
+    }
+    if (c->timing && (e = hipEventRecord(c->ev_mid, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    AdamWArgs a;
+    std::memset(&a, 0, sizeof(a));
+    for (int k = 0; k < b->k; ++k) {
+        a.params[k] = b->params[k];
+        a.exp_avg[k] = b->exp_avg[k];
+        a.exp_avg_sq[k] = b->exp_avg_sq[k];
+        a.grads[k] = b->grads[k];
+        a.copy[k] = static_cast<uint16_t*>(b->model_bf16[k]);
+    }
+    a.n = b->n;
+    a.norm_sq = clip ? c->sums : nullptr;
+    a.max_norm = co->max_grad_norm;
+    a.decay = static_cast<float>(1.0 - co->lr * co->weight_decay);
+    a.beta1 = static_cast<float>(co->beta1);
+    a.beta2 = static_cast<float>(co->beta2);
+    a.omb1 = static_cast<float>(1.0 - co->beta1);
+    a.omb2 = static_cast<float>(1.0 - co->beta2);
+    const double t = static_cast<double>(co->step);
+    a.step_size = static_cast<float>(co->lr / (1.0 - std::pow(co->beta1, t)));
+    a.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - std::pow(co->beta2, t)));
+    a.eps = static_cast<float>(co->eps);
+    e = launch_adamw(copy, b->k, adamw_blocks(c, b->n, b->k), c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "AdamW launch");
+    if (c->timing) {
+        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+        c->timed_valid = true;
+        c->adamw_timed = true;
+        c->adamw_norm_ran = norm_pass;
+    }
+    if (out != nullptr) {
+        e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double) * b->k, hipMemcpyDeviceToHost, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync");
+        e = hipStreamSynchronize(c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        finish_adamw(c->host_sums, b->k, co->max_grad_norm, out);
+    }
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+int autoloco_last_adamw_ms(autoloco_ctx* c, float* norm_ms, float* update_ms) {
+    if (c == nullptr || norm_ms == nullptr || update_ms == nullptr) return AUTOLOCO_E_INVALID;
+    if (!c->timed_valid || !c->adamw_timed) return fail(c, AUTOLOCO_E_STATE, "no timed AdamW step yet");
+    DeviceGuard g(c->device);
+    hipError_t e = hipEventSynchronize(c->ev_stop);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
+    *norm_ms = 0.0f;
+    if (c->adamw_norm_ran && (e = hipEventElapsedTime(norm_ms, c->ev_start, c->ev_mid)) != hipSuccess)
+        return hip_fail(c, e, "hipEventElapsedTime");
+    if ((e = hipEventElapsedTime(update_ms, c->ev_mid, c->ev_stop)) != hipSuccess)
+        return hip_fail(c, e, "hipEventElapsedTime");
     return AUTOLOCO_OK;
 }
 
