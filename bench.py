@@ -27,8 +27,12 @@ if ROOT not in sys.path:
 METRIC = "sync-round params/s and achieved HBM GB/s (% of peak), 1.1B params K=8"
 PEAK_HBM_GBS = 8000.0
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_36662_amd", "csrc", f)
-                  for f in ("round_kernels.hpp", "reduce.hpp", "round_inst.hip")]
+CSRC = os.path.join(ROOT, "paper_2609_36662_amd", "csrc")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("round_kernels.hpp", "reduce.hpp", "round_inst.hip")]
+INT8_SOURCES = KERNEL_SOURCES + [os.path.join(CSRC, f) for f in ("int8_kernels.hpp", "int8_inst.hip")]
+ADAMW_SOURCES = [os.path.join(CSRC, f) for f in ("adamw_kernels.hpp", "adamw_inst.hip", "round_kernels.hpp",
+                                                  "reduce.hpp")]
+INNER_METRIC = "inner AdamW step worker-params/s and achieved HBM GB/s (% of peak), 1.1B params K=8"
 
 # name -> (shape, K, replica dtype, recipe, selected horizon, base horizon)
 WORKLOADS = {
@@ -44,15 +48,15 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=None) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in sources or KERNEL_SOURCES:
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def committed_traffic(tag: str):
+def committed_traffic(tag: str, sources=None):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this
     kernel, if it was taken on the current kernel source; else None."""
     path = os.path.join(PROFILE_DIR, f"{tag}_traffic.txt")
@@ -64,7 +68,7 @@ def committed_traffic(tag: str):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash(sources):
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -130,6 +134,187 @@ def host_threads() -> int:
     return max(1, min(16, p))
 
 
+def copy_ceiling(torch, dev) -> float:
+    """GB/s of a 4 GiB device-to-device copy (median of five after one warm-up);
+    also the calibration kernel of the HBM byte counters."""
+    nbytes = 4 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    times = []
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del src, dst
+    gbs = 2 * nbytes / (statistics.median(times[1:]) * 1e-3) / 1e9
+    log(f"device-to-device copy of 4 GiB: {gbs:.0f} GB/s")
+    return gbs
+
+
+def inner_cpu_baseline(sample, lr, step, seconds: float, desc: str, threads: int = 1):
+    """The float64 oracle's inner step on a bounded sample: every worker's first
+    parameters, one worker per task (on a pool of threads when threads > 1)."""
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import adamw as oa
+    params, m, v, g = sample
+    n, k = params[0].shape[0], len(params)
+    cfg = oa.AdamWConfig()
+
+    def worker(i):
+        return oa.inner_step([params[i]], [m[i]], [v[i]], [g[i]], lr, step, cfg)
+
+    pool = ThreadPoolExecutor(threads) if threads > 1 else None
+    try:
+        done = 0
+        t0 = time.perf_counter()
+        while True:
+            if pool is not None:
+                list(pool.map(worker, range(k)))
+            else:
+                for i in range(k):
+                    worker(i)
+            done += n * k
+            if time.perf_counter() - t0 >= seconds:
+                break
+        dt = time.perf_counter() - t0
+    finally:
+        if pool is not None:
+            pool.shutdown()
+    how = "one thread" if threads == 1 else f"one worker per task on {threads} threads"
+    return {"value": done / dt, "unit": "worker-params/s", "cores": threads, "kind": "oracle",
+            "sample": f"{desc}: first {n:,} parameters of each of {k} workers (clipping on the sample's own "
+                      f"norm), step repeated {done // (n * k)}x over {dt:.1f} s (numpy float64, {how})"}
+
+
+def bench_inner(args) -> int:
+    """One AdamW step of every worker (gradient-norm pass + update pass) per timed step."""
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import inner, shapes
+
+    shape_name, k = WORKLOADS[args.workload][0], WORKLOADS[args.workload][1]
+    if args.k:
+        k = args.k
+    n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    update_bytes = n * k * (28 + (2 if args.copy else 0))
+    norm_bytes = n * k * 4
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sched = al.make_schedule()
+    s0 = 20_000
+    log(f"inner step {args.workload}: n={n:,} K={k} update bytes={update_bytes / 1e9:.3f} GB "
+        f"norm bytes={norm_bytes / 1e9:.3f} GB")
+    ctx = al.autoloco_create(0)
+    t = time.perf_counter()
+    dtypes = [torch.float32] * (4 * k) + ([torch.bfloat16] * k if args.copy else [])
+    spread = False
+    if args.alloc == "spread":
+        ts, spread = al.spread_tensors(ctx, n, dtypes)
+    else:
+        ts = [torch.empty(n, dtype=d, device=dev) for d in dtypes]
+    st = inner.InnerState(ts[0:k], ts[k:2 * k], ts[2 * k:3 * k], ts[3 * k:4 * k])
+    copies = ts[4 * k:5 * k] if args.copy else None
+    inner.fill_state(st, seed=42)
+    inner.fill_grads(st, seed=42, step=0)
+    torch.cuda.synchronize()
+    log(f"buffers ({args.alloc}{', spread' if spread else ''}) allocated and filled in "
+        f"{time.perf_counter() - t:.1f} s")
+
+    sample = None
+    if not args.no_cpu_baseline:
+        s = min(n, args.cpu_sample // 4)
+        sample = tuple([t_[:s].cpu().numpy().astype("float64") for t_ in grp]
+                       for grp in (st.params, st.exp_avg, st.exp_avg_sq, st.grads))
+
+    if args.grid:
+        al.autoloco_set_grid_limit(ctx, args.grid)
+    al.autoloco_set_timing(ctx, True)
+    step_no = [1000]
+
+    def one_step():
+        lr = al.autoloco_inner_lr(sched, s0 + step_no[0])
+        co = al.make_adamw_coeffs(lr, step_no[0])
+        out = al.autoloco_inner_adamw(ctx, st.params, st.exp_avg, st.exp_avg_sq, st.grads, co, model_bf16=copies)
+        step_no[0] += 1
+        return out, al.autoloco_last_adamw_ms(ctx)
+
+    first = None
+    for i in range(args.warmup):
+        out, _ = one_step()
+        if i == 0:
+            first = out
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    norm_ms, upd_ms = [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        _, (a, b) = one_step()
+        norm_ms.append(a)
+        upd_ms.append(b)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    upd_mean, norm_mean = statistics.mean(upd_ms), statistics.mean(norm_ms)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step wall; update pass {upd_mean:.3f} ms "
+        f"({update_bytes / upd_mean / 1e6:.0f} GB/s), norm pass {norm_mean:.3f} ms "
+        f"({norm_bytes / norm_mean / 1e6:.0f} GB/s)")
+    ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
+    achieved = update_bytes / (upd_mean * 1e-3) / 1e9
+    tag = f"adamw_f32_k{k}_{args.workload}" + ("_copy" if args.copy else "")
+    traffic = committed_traffic(tag, ADAMW_SOURCES)
+
+    cpu = cpu1 = None
+    if sample is not None:
+        desc = f"{args.workload} K={k} inner AdamW"
+        p = host_threads()
+        lr = al.autoloco_inner_lr(sched, s0)
+        log(f"timing the oracle on the CPU sample: one thread, then {min(p, k)} threads")
+        cpu1 = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc)
+        cpu = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc, threads=min(p, k)) \
+            if min(p, k) > 1 else cpu1
+
+    out = {
+        "metric": INNER_METRIC,
+        "value": n * k / (ms_per_step * 1e-3),
+        "unit": "worker-params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload} inner AdamW step: {n:,} parameters x K={k} workers, fp32 master "
+                        f"parameters, moments and gradients, per-worker gradient-norm clipping 1.0, "
+                        f"betas (0.9, 0.95), weight decay 0.1" + (", BF16 compute copy" if args.copy else ""),
+            "n_params": n, "k": k, "update_bytes": update_bytes, "norm_bytes": norm_bytes,
+            "alloc": args.alloc + (" (spread)" if spread else ""),
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": "adamw_kernel (update pass)",
+        },
+        "update_ms_mean": upd_mean,
+        "norm_ms_mean": norm_mean,
+        "norm_pass_gbs": norm_bytes / (norm_mean * 1e-3) / 1e9,
+        "copy_ceiling_gbs": ceiling,
+        "first_step_grad_norms": list(first.grad_norm[:k]) if first is not None else None,
+        "cpu_baseline": cpu,
+        "cpu_baseline_one_thread": cpu1,
+        "kernel_source_sha256_16": kernel_source_hash(ADAMW_SOURCES),
+    }
+    print(json.dumps(out), flush=True)
+    del st, copies, ts
+    ctx.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -148,12 +333,18 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
     ap.add_argument("--perturbed", type=int, default=3, help="extra rounds on freshly drawn replicas")
+    ap.add_argument("--step", choices=("round", "inner"), default="round",
+                    help="round: the synchronisation round; inner: one AdamW step of every worker")
+    ap.add_argument("--copy", action="store_true", help="inner: also write each worker's BF16 compute copy")
     args = ap.parse_args()
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the round keeps all K replicas on one device and has no "
               f"multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         return 2
+
+    if args.step == "inner":
+        return bench_inner(args)
 
     import torch
     import paper_2609_36662_amd as al
@@ -250,27 +441,12 @@ def main() -> int:
     if perturbed_ms:
         log(f"rounds on freshly drawn replicas: kernel {statistics.median(perturbed_ms):.3f} ms (median)")
 
-    ceiling = None
-    if not args.no_ceiling:
-        nbytes = 4 << 30
-        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        times = []
-        for _ in range(6):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            dst.copy_(src)
-            e1.record()
-            e1.synchronize()
-            times.append(e0.elapsed_time(e1))
-        ceiling = 2 * nbytes / (statistics.median(times[1:]) * 1e-3) / 1e9
-        del src, dst
-        log(f"device-to-device copy of 4 GiB: {ceiling:.0f} GB/s")
+    ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
 
     mean_ms = statistics.mean(kernel_ms)
     achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
     tag = f"round_{rdt}_k{k}_{args.workload}" + ("_int8" if args.codec == "int8" else "")
-    traffic = committed_traffic(tag)
+    traffic = committed_traffic(tag, INT8_SOURCES if args.codec == "int8" else None)
 
     cpu = cpu1 = None
     if sample is not None:
@@ -315,7 +491,7 @@ def main() -> int:
         if first_stats else None,
         "cpu_baseline": cpu,
         "cpu_baseline_one_thread": cpu1,
-        "kernel_source_sha256_16": kernel_source_hash(),
+        "kernel_source_sha256_16": kernel_source_hash(INT8_SOURCES if args.codec == "int8" else None),
     }
     print(json.dumps(out), flush=True)
     del inp
