@@ -27,6 +27,8 @@ Modules
                 "Adaptive Interval Selection"; App. A).
   int8_codec  — the INT8 blockwise pseudo-gradient codec and the round that
                 averages through it (App. G.1).
+  bf16_payload — the round whose worker average travels as BF16
+                pseudo-gradients (the payload of the paper's main runs).
   adamw       — one inner AdamW step of every worker with its own
                 gradient-norm clipping (Table "Training settings"; App. G.1).
 
