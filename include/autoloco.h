@@ -200,6 +200,22 @@ int autoloco_outer_step_int8(autoloco_ctx* ctx, const autoloco_buffers* bufs,
                              const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
                              autoloco_stats* out, int8_t* mean_codes, float* mean_scales);
 
+/* The same corrected Nesterov step, with the worker average taken as the
+ * paper's main runs communicate it: BF16 pseudo-gradients (Table "Quality and
+ * communication cost": payload in full-model BF16 tensors per worker; App.
+ * G.1: master parameters, outer reference and momentum stay FP32).  Per
+ * parameter: Delta_k = theta - theta_k in FP32, each rounded to BF16 (nearest
+ * even); their sum in float64 in worker order times 1/K, rounded to FP32 and
+ * then to BF16, is the mean every worker receives, and the step uses it.
+ * Statistics (FUSE_STATS): sq_norm from the unrounded Delta_k (D), sq_mean
+ * from the received mean (C), sq_dev = ||Delta_k - received mean||^2.
+ * mean_bf16 ([n] bf16 bit patterns, 16-byte aligned) receives the received
+ * mean, or NULL.  Flags, blocking and non-finite data as autoloco_outer_step.
+ * Errors: as autoloco_outer_step, plus E_ALIGN / E_ALIAS for mean_bf16. */
+int autoloco_outer_step_bf16(autoloco_ctx* ctx, const autoloco_buffers* bufs,
+                             const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
+                             autoloco_stats* out, uint16_t* mean_bf16);
+
 /* Replica reset alone: theta_k <- theta for every replica (Alg. "AutoLoCo
  * outer interval", start of the local loop).  Asynchronous on the stream.
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */

@@ -12,7 +12,7 @@ from ._lib import (  # noqa: F401
     autoloco_alloc_spread, autoloco_broadcast_reset, autoloco_controller_create, autoloco_free, autoloco_controller_load,
     autoloco_controller_reference, autoloco_controller_save, autoloco_create, autoloco_destroy,
     autoloco_inner_lr, autoloco_last_error, autoloco_last_kernel_ms, autoloco_launch_shape,
-    autoloco_lr_mass, autoloco_outer_correction, autoloco_outer_step, autoloco_outer_step_int8, autoloco_round_stats,
+    autoloco_lr_mass, autoloco_outer_correction, autoloco_outer_step, autoloco_outer_step_bf16, autoloco_outer_step_int8, autoloco_round_stats,
     autoloco_select_interval, autoloco_set_grid_limit, autoloco_set_timing, default_controller_cfg,
     lib, make_buffers, make_coeffs, make_observation, make_outer_cfg, make_schedule, spread_tensors,
     autoloco_inner_adamw, autoloco_last_adamw_ms, make_adamw_buffers, make_adamw_coeffs,

@@ -133,6 +133,8 @@ SYMBOLS = [
                                       C.c_uint32, C.c_double, C.POINTER(Stats)]),
     ("autoloco_outer_step_int8", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p, C.c_void_p]),
+    ("autoloco_outer_step_bf16", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
+                                           C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_inner_adamw", C.c_int, [C.c_void_p, C.POINTER(AdamWBuffers), C.POINTER(AdamWCoeffs),
                                        C.POINTER(AdamWStats)]),
@@ -400,6 +402,25 @@ def autoloco_outer_step_int8(ctx: Context, theta, momentum, replicas, coeffs: Ou
                                           C.c_void_p(mean_scales.data_ptr()) if mean_scales is not None else None),
            "autoloco_outer_step_int8", ctx)
     return out if flags & FUSE_STATS else None
+
+
+def autoloco_outer_step_bf16(ctx: Context, theta, momentum, replicas, coeffs: OuterCoeffs,
+                             flags: int = FUSE_STATS | FUSE_RESET, eps: float = 1e-12, mean_bf16=None,
+                             n=None) -> Optional[Stats]:
+    """The round with BF16 pseudo-gradient payloads; mean_bf16 (a bfloat16 tensor
+    of at least n elements) receives the mean every worker receives."""
+    import torch
+    b = make_buffers(theta, replicas, momentum, n)
+    if mean_bf16 is not None:
+        if not isinstance(mean_bf16, torch.Tensor) or mean_bf16.device.type != "cuda" \
+                or mean_bf16.dtype != torch.bfloat16 or not mean_bf16.is_contiguous() or mean_bf16.numel() < b.n:
+            raise ValueError("mean_bf16 must be a contiguous CUDA bfloat16 tensor of at least n elements")
+    st = Stats() if flags & FUSE_STATS else None
+    _check(lib().autoloco_outer_step_bf16(ctx.handle, C.byref(b), C.byref(coeffs), int(flags), float(eps),
+                                          C.byref(st) if st is not None else None,
+                                          C.c_void_p(mean_bf16.data_ptr()) if mean_bf16 is not None else None),
+           "autoloco_outer_step_bf16", ctx)
+    return st
 
 
 def autoloco_broadcast_reset(ctx: Context, theta, replicas, n=None) -> None:

@@ -50,7 +50,7 @@ def jobs():
     hipcc = _hipcc()
     cmds = []
     for rt, rtname in ((0, "f32"), (1, "bf16")):
-        for mode in range(5):
+        for mode in range(9):
             obj = os.path.join(BUILD, f"round_{rtname}_m{mode}.o")
             cmds.append([hipcc, *HIP_FLAGS, f"-DAL_RT={rt}", f"-DAL_RTNAME={rtname}", f"-DAL_MODE={mode}",
                          "-c", os.path.join(CSRC, "round_inst.hip"), "-o", obj])

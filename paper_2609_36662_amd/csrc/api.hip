@@ -30,6 +30,7 @@ struct autoloco_ctx {
     int grid_limit = 0;
     int occupancy[2][AUTOLOCO_MAX_K + 1] = {};  // resident workgroups per CU, by replica type and k
     int occupancy_int8[2][AUTOLOCO_MAX_K + 1] = {};
+    int occupancy_bf16p[2][AUTOLOCO_MAX_K + 1] = {};  // the BF16-payload round
     double* partials = nullptr;
     unsigned int* ticket = nullptr;
     double* sums = nullptr;
@@ -77,10 +78,10 @@ size_t replica_size(int32_t dtype) { return dtype == AUTOLOCO_BF16 ? 2 : 4; }
 // slowest by 5-9 %.  Every mode of a given (k, replica type) uses the same
 // grid, so the statistics of a standalone and of a fused call are summed in
 // the same order, bit for bit.
-int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k) {
+int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k, bool bf16p = false) {
     const int64_t v = dtype == AUTOLOCO_BF16 ? 8 : 4;
     const int64_t nvec = n / v;
-    int per_cu = ctx->occupancy[dtype == AUTOLOCO_BF16 ? 1 : 0][k];
+    int per_cu = (bf16p ? ctx->occupancy_bf16p : ctx->occupancy)[dtype == AUTOLOCO_BF16 ? 1 : 0][k];
     if (per_cu > 3) per_cu = 3;
     if (per_cu < 1) per_cu = 1;
     int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * per_cu;
@@ -163,10 +164,13 @@ void finish_stats(const double* sums, int k, double eps, autoloco_stats* out) {
 
 RoundLauncher launcher(int32_t dtype, int mode) {
     static const RoundLauncher f32[MODE_COUNT] = {launch_round_f32_m0, launch_round_f32_m1, launch_round_f32_m2,
-                                                  launch_round_f32_m3, launch_round_f32_m4};
+                                                  launch_round_f32_m3, launch_round_f32_m4, launch_round_f32_m5,
+                                                  launch_round_f32_m6, launch_round_f32_m7, launch_round_f32_m8};
     static const RoundLauncher bf16[MODE_COUNT] = {launch_round_bf16_m0, launch_round_bf16_m1,
                                                    launch_round_bf16_m2, launch_round_bf16_m3,
-                                                   launch_round_bf16_m4};
+                                                   launch_round_bf16_m4, launch_round_bf16_m5,
+                                                   launch_round_bf16_m6, launch_round_bf16_m7,
+                                                   launch_round_bf16_m8};
     return dtype == AUTOLOCO_BF16 ? bf16[mode] : f32[mode];
 }
 
@@ -191,7 +195,7 @@ RoundArgs make_args(autoloco_ctx* ctx, const autoloco_buffers* b) {
 // sums and fills *out.
 int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, int mode, bool stats,
               double eps, autoloco_stats* out) {
-    const int blocks = blocks_for(ctx, b->n, b->replica_dtype, b->k);
+    const int blocks = blocks_for(ctx, b->n, b->replica_dtype, b->k, mode >= MODE_P_UPDATE);
     hipError_t e;
     if (ctx->timing && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
@@ -295,6 +299,8 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
         c->occupancy[1][k] = occupancy_round_bf16_m4(k);
         c->occupancy_int8[0][k] = occupancy_int8_f32_s1r1(k);
         c->occupancy_int8[1][k] = occupancy_int8_bf16_s1r1(k);
+        c->occupancy_bf16p[0][k] = occupancy_round_f32_m8(k);
+        c->occupancy_bf16p[1][k] = occupancy_round_bf16_m8(k);
     }
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
               hipMalloc(&c->ticket, 256) == hipSuccess &&
@@ -405,6 +411,48 @@ int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autolo
     a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
     const int mode = stats ? (reset ? MODE_UPDATE_STATS_RESET : MODE_UPDATE_STATS)
                            : (reset ? MODE_UPDATE_RESET : MODE_UPDATE);
+    return run_round(c, b, a, mode, stats, eps, out);
+}
+
+int autoloco_outer_step_bf16(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
+                             uint32_t flags, double eps, autoloco_stats* out, uint16_t* mean_bf16) {
+    int st = validate(c, b, true);
+    if (st != AUTOLOCO_OK) return st;
+    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
+    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
+    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
+    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
+    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
+    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
+        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    if (b->n == 0) {
+        if (stats) zero_stats(b->k, eps, out);
+        return AUTOLOCO_OK;
+    }
+    if (mean_bf16 != nullptr) {
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(mean_bf16), hi = lo + static_cast<uintptr_t>(b->n) * 2u;
+        if (lo % 16 != 0) return fail(c, AUTOLOCO_E_ALIGN, "mean_bf16 not 16-byte aligned");
+        const uintptr_t fbytes = static_cast<uintptr_t>(b->n) * 4u;
+        const uintptr_t rbytes = static_cast<uintptr_t>(b->n) * replica_size(b->replica_dtype);
+        auto hit = [&](const void* p, uintptr_t len) {
+            const uintptr_t q = reinterpret_cast<uintptr_t>(p);
+            return lo < q + len && q < hi;
+        };
+        bool alias = hit(b->theta, fbytes) || hit(b->momentum, fbytes);
+        for (int k = 0; k < b->k; ++k) alias = alias || hit(b->replicas[k], rbytes);
+        if (alias) return fail(c, AUTOLOCO_E_ALIAS, "mean_bf16 overlaps a round buffer");
+    }
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RoundArgs a = make_args(c, b);
+    a.mu = static_cast<float>(co->mu);
+    a.eta = static_cast<float>(co->eta_out);
+    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    a.payload = mean_bf16;
+    a.inv_k64 = 1.0 / static_cast<double>(b->k);
+    const int mode = stats ? (reset ? MODE_P_UPDATE_STATS_RESET : MODE_P_UPDATE_STATS)
+                           : (reset ? MODE_P_UPDATE_RESET : MODE_P_UPDATE);
     return run_round(c, b, a, mode, stats, eps, out);
 }
 

@@ -1,5 +1,5 @@
 // One (replica type, mode) slice of the round kernels, for every K.
-// Compiled once per slice with -DAL_RT=<0|1> -DAL_RTNAME=<f32|bf16> -DAL_MODE=<0..4>,
+// Compiled once per slice with -DAL_RT=<0|1> -DAL_RTNAME=<f32|bf16> -DAL_MODE=<0..8>,
 // so the template instances build in parallel.
 #include "round_kernels.hpp"
 
@@ -14,13 +14,15 @@
 namespace autoloco {
 namespace {
 
-constexpr bool kStats = AL_MODE == MODE_STATS || AL_MODE == MODE_UPDATE_STATS || AL_MODE == MODE_UPDATE_STATS_RESET;
-constexpr bool kUpdate = AL_MODE != MODE_STATS;
-constexpr bool kReset = AL_MODE == MODE_UPDATE_RESET || AL_MODE == MODE_UPDATE_STATS_RESET;
+constexpr bool kBf16p = AL_MODE >= MODE_P_UPDATE;
+constexpr int kBase = kBf16p ? AL_MODE - 4 : AL_MODE;   // the plain mode with the same outputs
+constexpr bool kStats = kBase == MODE_STATS || kBase == MODE_UPDATE_STATS || kBase == MODE_UPDATE_STATS_RESET;
+constexpr bool kUpdate = kBase != MODE_STATS;
+constexpr bool kReset = kBase == MODE_UPDATE_RESET || kBase == MODE_UPDATE_STATS_RESET;
 
 template <int K>
 hipError_t launch_k(int blocks, hipStream_t stream, const RoundArgs& a) {
-    hipLaunchKernelGGL((round_kernel<K, AL_RT, kStats, kUpdate, kReset>), dim3(blocks), dim3(kBlock), 0, stream,
+    hipLaunchKernelGGL((round_kernel<K, AL_RT, kStats, kUpdate, kReset, kBf16p>), dim3(blocks), dim3(kBlock), 0, stream,
                        a);
     return hipGetLastError();
 }
@@ -28,7 +30,7 @@ hipError_t launch_k(int blocks, hipStream_t stream, const RoundArgs& a) {
 template <int K>
 int occ_k() {
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, round_kernel<K, AL_RT, kStats, kUpdate, kReset>, kBlock,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, round_kernel<K, AL_RT, kStats, kUpdate, kReset, kBf16p>, kBlock,
                                                      0) != hipSuccess)
         return 0;
     return blocks;

@@ -35,10 +35,14 @@ constexpr int kBlock = 256;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2r __attribute__((ext_vector_type(2)));
 
 enum ReplicaType { RT_F32 = 0, RT_BF16 = 1 };
+// Modes 5..8 are modes 1..4 with the worker average taken through BF16
+// pseudo-gradient payloads.
 enum Mode { MODE_STATS = 0, MODE_UPDATE = 1, MODE_UPDATE_STATS = 2, MODE_UPDATE_RESET = 3,
-            MODE_UPDATE_STATS_RESET = 4, MODE_COUNT = 5 };
+            MODE_UPDATE_STATS_RESET = 4, MODE_P_UPDATE = 5, MODE_P_UPDATE_STATS = 6, MODE_P_UPDATE_RESET = 7,
+            MODE_P_UPDATE_STATS_RESET = 8, MODE_COUNT = 9 };
 
 struct RoundArgs {
     float* theta;
@@ -49,6 +53,8 @@ struct RoundArgs {
     double* partials;      // [gridDim.x][2K+1]
     unsigned int* ticket;  // zero between launches
     double* sums;          // [2K+1] final sums
+    uint16_t* payload;     // BF16 payload modes: [n] bits of the received mean, or null
+    double inv_k64;        // 1/K in float64 (BF16 payload modes)
 };
 
 // ------------------------------------------------------------------ memory --
@@ -106,15 +112,28 @@ __device__ __forceinline__ float tree_sum(const float (&d)[K]) {
 }
 
 // One parameter: pseudo-gradients, their mean, the squared-sum terms and the
-// corrected Nesterov step.
-template <int K, bool STATS, bool UPDATE>
+// corrected Nesterov step.  With BF16P the mean is the one every worker
+// receives when the pseudo-gradients travel as BF16: each Delta_k rounded to
+// BF16 (nearest even), their float64 sum in worker order times float64(1/K)
+// rounded to FP32, then to BF16 (its bits go to pb); the squared sums use the
+// unrounded Delta_k and that received mean.
+template <int K, bool STATS, bool UPDATE, bool BF16P>
 __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K], const RoundArgs& a,
                                           float (&s)[K], float (&q)[K], float& m, float& th_new,
-                                          float& v_new) {
+                                          float& v_new, uint32_t& pb) {
     float d[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) d[k] = th - r[k];
-    const float mean = tree_sum<0, K, K>(d) * a.inv_k;
+    float mean;
+    if constexpr (BF16P) {
+        double sum = 0.0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) sum += (double)__uint_as_float(bf16_rne(d[k]) << 16);
+        pb = bf16_rne((float)(sum * a.inv_k64));
+        mean = __uint_as_float(pb << 16);
+    } else {
+        mean = tree_sum<0, K, K>(d) * a.inv_k;
+    }
     if constexpr (STATS) {
 #pragma unroll
         for (int k = 0; k < K; ++k) {
@@ -133,7 +152,7 @@ __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K]
 }
 
 // ------------------------------------------------------------ round kernel --
-template <int K, int RT, bool STATS, bool UPDATE, bool RESET>
+template <int K, int RT, bool STATS, bool UPDATE, bool RESET, bool BF16P = false>
 __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
     constexpr int V = RT == RT_F32 ? 4 : 8;  // parameters per 16-byte replica vector
     constexpr int NS = STATS ? 2 * K + 1 : 1;
@@ -206,12 +225,27 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
 #pragma unroll
         for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
         float th_new[V], v_new[V];
+        uint32_t pb[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) {
             float re[K];
 #pragma unroll
             for (int k = 0; k < K; ++k) re[k] = r[k][e];
-            one_param<K, STATS, UPDATE>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e]);
+            one_param<K, STATS, UPDATE, BF16P>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e], pb[e]);
+        }
+        if constexpr (BF16P) {
+            if (a.payload != nullptr) {
+                // 2 bytes per parameter: 8 (fp32 replicas) or 16 bytes per lane
+                char* const pw = reinterpret_cast<char*>(a.payload + wb);
+                const uint32_t po = threadIdx.x * (uint32_t)V * 2u;
+                if constexpr (V == 4)
+                    __builtin_nontemporal_store(u32x2r{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16},
+                                                reinterpret_cast<u32x2r*>(pw + po));
+                else
+                    __builtin_nontemporal_store(u32x4{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16, pb[4] | pb[5] << 16,
+                                                      pb[6] | pb[7] << 16},
+                                                reinterpret_cast<u32x4*>(pw + po));
+            }
         }
         if constexpr (STATS) {
 #pragma unroll
@@ -260,9 +294,13 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
                 r[k] = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.replicas[k])[j] << 16);
         }
         float s[K], q[K], m = 0.f, th_new = 0.f, v_new = 0.f;
+        uint32_t pb = 0;
 #pragma unroll
         for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
-        one_param<K, STATS, UPDATE>(th, v, r, a, s, q, m, th_new, v_new);
+        one_param<K, STATS, UPDATE, BF16P>(th, v, r, a, s, q, m, th_new, v_new, pb);
+        if constexpr (BF16P) {
+            if (a.payload != nullptr) a.payload[j] = (uint16_t)pb;
+        }
         if constexpr (STATS) {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
@@ -337,9 +375,19 @@ hipError_t launch_round_bf16_m1(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m2(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m3(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m4(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m5(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m6(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m7(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_f32_m8(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m5(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m6(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m7(int, int, hipStream_t, const RoundArgs&);
+hipError_t launch_round_bf16_m8(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_reset(int rt, int k, int blocks, hipStream_t stream, const RoundArgs& a);
 // Resident workgroups per compute unit of the fused (update + stats + reset) kernel.
 int occupancy_round_f32_m4(int k);
 int occupancy_round_bf16_m4(int k);
+int occupancy_round_f32_m8(int k);
+int occupancy_round_bf16_m8(int k);
 
 }  // namespace autoloco
