@@ -323,9 +323,11 @@ def main() -> int:
     ap.add_argument("--workload", default="llama-1.1b", choices=sorted(WORKLOADS))
     ap.add_argument("--grid", type=int, default=0, help="cap on workgroups (0 = library default)")
     ap.add_argument("--k", type=int, default=0, help="override the workload's replica count")
-    ap.add_argument("--codec", choices=("fp32", "int8"), default="fp32",
-                    help="int8: the worker average travels through the INT8 blockwise codec")
-    ap.add_argument("--payload", action="store_true", help="int8: also write the encoded mean (codes + scales)")
+    ap.add_argument("--codec", choices=("fp32", "int8", "bf16"), default="fp32",
+                    help="int8: the worker average travels through the INT8 blockwise codec; "
+                         "bf16: as BF16 pseudo-gradient payloads")
+    ap.add_argument("--payload", action="store_true",
+                    help="int8 / bf16: also write the mean every worker receives (codes + scales, or BF16)")
     ap.add_argument("--alloc", choices=("spread", "torch"), default="spread",
                     help="spread: the library's placement-aware allocator; torch: torch.empty")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -402,11 +404,17 @@ def main() -> int:
         codes = torch.empty(n, dtype=torch.int8, device=dev)
         scales = torch.empty((n + 4095) // 4096, dtype=torch.float32, device=dev)
         bytes_per_round += n + 4 * ((n + 4095) // 4096)
+    if args.codec == "bf16" and args.payload:
+        codes = torch.empty(n, dtype=torch.bfloat16, device=dev)
+        bytes_per_round += 2 * n
 
     def one_round():
         if args.codec == "int8":
             st = al.autoloco_outer_step_int8(ctx, inp.theta, inp.momentum, inp.replicas, coeffs, flags, 1e-12,
                                              mean_codes=codes, mean_scales=scales)
+        elif args.codec == "bf16":
+            st = al.autoloco_outer_step_bf16(ctx, inp.theta, inp.momentum, inp.replicas, coeffs, flags, 1e-12,
+                                             mean_bf16=codes)
         else:
             st = al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, coeffs, flags, 1e-12)
         return st, al.autoloco_last_kernel_ms(ctx)
@@ -445,7 +453,7 @@ def main() -> int:
 
     mean_ms = statistics.mean(kernel_ms)
     achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
-    tag = f"round_{rdt}_k{k}_{args.workload}" + ("_int8" if args.codec == "int8" else "")
+    tag = f"round_{rdt}_k{k}_{args.workload}" + ("" if args.codec == "fp32" else f"_{args.codec}")
     traffic = committed_traffic(tag, INT8_SOURCES if args.codec == "int8" else None)
 
     cpu = cpu1 = None
@@ -472,9 +480,10 @@ def main() -> int:
         "config": {
             "workload": f"{args.workload}: {n:,} parameters as one flat arena per buffer, K={k} "
                         f"{rdt} replicas, fp32 theta and momentum, fused stats + Nesterov + reset"
-                        + (", worker average through the INT8 blockwise codec" if args.codec == "int8" else ""),
+                        + {"fp32": "", "int8": ", worker average through the INT8 blockwise codec",
+                           "bf16": ", worker average as BF16 pseudo-gradient payloads"}[args.codec],
             "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
-            "grid": [blocks, threads], "alloc": args.alloc + (" (spread)" if spread else ""),
+            "grid": [blocks, threads] if args.codec == "fp32" else None, "alloc": args.alloc + (" (spread)" if spread else ""),
             "codec": args.codec + (" + payload" if codes is not None else ""),
             "h_selected": h_sel, "h_base": h_base,
             "rho": coeffs.rho, "mu": coeffs.mu, "eta_out": coeffs.eta_out,
