@@ -222,6 +222,51 @@ int autoloco_outer_step_bf16(autoloco_ctx* ctx, const autoloco_buffers* bufs,
 int autoloco_broadcast_reset(autoloco_ctx* ctx, const autoloco_buffers* bufs);
 
 /* ------------------------------------------------------------------------ */
+/* One GPU's share of a round with one worker replica per GPU                */
+/* ------------------------------------------------------------------------ */
+
+/* In the paper's topology every worker's replica lives on its own GPU and the
+ * pseudo-gradients travel as BF16 payloads.  A round then is, on GPU r:
+ *   1. autoloco_rank_payload: Delta_r = theta - theta_r (FP32) as a BF16
+ *      payload, and ||Delta_r||^2 (D = the mean over workers of these);
+ *   2. an all-to-all of payload shards (GPU s receives shard s of every
+ *      worker's payload; not part of this library);
+ *   3. autoloco_shard_step on GPU r's shard: the received mean and the
+ *      corrected Nesterov step of theta and v on that shard, and the shard's
+ *      ||mean||^2 (C = K * (sum over shards) / (D + eps));
+ *   4. an all-gather of theta' shards into theta, and autoloco_broadcast_reset
+ *      for the worker's replica.
+ * Steps 1 and 3 use the arithmetic of autoloco_outer_step_bf16, so theta',
+ * v' and the received mean equal that call's bit for bit. */
+
+/* Step 1 for one worker.  theta: [n] fp32; replica: [n] fp32 or bf16
+ * (replica_dtype); payload: [n] bf16 bit patterns, written.  All 16-byte
+ * aligned and disjoint.  sq_norm (or NULL) receives ||Delta_r||^2 (float64, deterministic
+ * order); with it the call blocks, without it it is asynchronous.
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_rank_payload(autoloco_ctx* ctx, int64_t n, const float* theta, const void* replica,
+                          int32_t replica_dtype, uint16_t* payload, double* sq_norm);
+
+/* Buffers of one GPU's shard: n parameters of theta and v (fp32, read and
+ * written) and the K workers' payload shards for them (bf16, read). */
+typedef struct {
+    int64_t n;
+    int32_t k;
+    float* theta;
+    float* momentum;
+    const uint16_t* payloads[AUTOLOCO_MAX_K];
+} autoloco_shard_buffers;
+
+/* Step 3 on one shard: mean = bf16(fp32(sum_k payload_k in float64, worker
+ * order, times 1/K)); the corrected Nesterov step with it (coefficients as
+ * autoloco_outer_step); mean_bf16 ([n], or NULL) receives the mean's bits;
+ * sq_mean (or NULL) receives the shard's ||mean||^2 and makes the call block.
+ * Errors: E_INVALID (k outside 1..16, null or non-finite arguments),
+ * E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_shard_step(autoloco_ctx* ctx, const autoloco_shard_buffers* bufs,
+                        const autoloco_outer_coeffs* coeffs, uint16_t* mean_bf16, double* sq_mean);
+
+/* ------------------------------------------------------------------------ */
 /* Inner AdamW step of the K workers                                         */
 /* ------------------------------------------------------------------------ */
 

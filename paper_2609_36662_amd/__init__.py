@@ -15,5 +15,5 @@ from ._lib import (  # noqa: F401
     autoloco_lr_mass, autoloco_outer_correction, autoloco_outer_step, autoloco_outer_step_bf16, autoloco_outer_step_int8, autoloco_round_stats,
     autoloco_select_interval, autoloco_set_grid_limit, autoloco_set_timing, default_controller_cfg,
     lib, make_buffers, make_coeffs, make_observation, make_outer_cfg, make_schedule, spread_tensors,
-    autoloco_inner_adamw, autoloco_last_adamw_ms, make_adamw_buffers, make_adamw_coeffs,
+    autoloco_inner_adamw, autoloco_last_adamw_ms, autoloco_rank_payload, autoloco_shard_step, make_adamw_buffers, make_adamw_coeffs,
 )

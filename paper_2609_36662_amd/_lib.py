@@ -94,6 +94,11 @@ class Decision(C.Structure):
                 ("done", C.c_int32), ("reserved", C.c_int32), ("coeffs", OuterCoeffs)]
 
 
+class ShardBuffers(C.Structure):
+    _fields_ = [("n", C.c_int64), ("k", C.c_int32), ("theta", C.c_void_p), ("momentum", C.c_void_p),
+                ("payloads", C.c_void_p * MAX_K)]
+
+
 class AdamWBuffers(C.Structure):
     _fields_ = [("n", C.c_int64), ("k", C.c_int32), ("params", C.c_void_p * MAX_K),
                 ("exp_avg", C.c_void_p * MAX_K), ("exp_avg_sq", C.c_void_p * MAX_K),
@@ -136,6 +141,10 @@ SYMBOLS = [
     ("autoloco_outer_step_bf16", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
+    ("autoloco_rank_payload", C.c_int, [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
+                                        C.POINTER(C.c_double)]),
+    ("autoloco_shard_step", C.c_int, [C.c_void_p, C.POINTER(ShardBuffers), C.POINTER(OuterCoeffs), C.c_void_p,
+                                      C.POINTER(C.c_double)]),
     ("autoloco_inner_adamw", C.c_int, [C.c_void_p, C.POINTER(AdamWBuffers), C.POINTER(AdamWCoeffs),
                                        C.POINTER(AdamWStats)]),
     ("autoloco_last_adamw_ms", C.c_int, [C.c_void_p, C.POINTER(C.c_float), C.POINTER(C.c_float)]),
@@ -421,6 +430,49 @@ def autoloco_outer_step_bf16(ctx: Context, theta, momentum, replicas, coeffs: Ou
                                           C.c_void_p(mean_bf16.data_ptr()) if mean_bf16 is not None else None),
            "autoloco_outer_step_bf16", ctx)
     return st
+
+
+def _cuda_contig(t, dtype, n, what):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or not t.is_contiguous() or t.dtype != dtype:
+        raise TypeError(f"{what} must be a contiguous CUDA {dtype} tensor")
+    if t.numel() < n:
+        raise ValueError(f"{what} is shorter than n")
+    return t.data_ptr()
+
+
+def autoloco_rank_payload(ctx: Context, theta, replica, payload, sq_norm: bool = True, n=None):
+    """One worker's BF16 payload (into `payload`) and ||Delta_r||^2 (or None)."""
+    import torch
+    count = theta.numel() if n is None else int(n)
+    code = _dtype_code(replica)
+    out = C.c_double() if sq_norm else None
+    _check(lib().autoloco_rank_payload(ctx.handle, count, _cuda_contig(theta, torch.float32, count, "theta"),
+                                       _cuda_contig(replica, replica.dtype, count, "replica"), code,
+                                       _cuda_contig(payload, torch.bfloat16, count, "payload"),
+                                       C.byref(out) if out is not None else None), "autoloco_rank_payload", ctx)
+    return out.value if out is not None else None
+
+
+def autoloco_shard_step(ctx: Context, theta, momentum, payloads: Sequence, coeffs: OuterCoeffs, mean_bf16=None,
+                        sq_mean: bool = True, n=None):
+    """The received mean and the corrected step on one shard; returns the shard's ||mean||^2 (or None)."""
+    import torch
+    count = theta.numel() if n is None else int(n)
+    if not 1 <= len(payloads) <= MAX_K:
+        raise ValueError(f"need 1..{MAX_K} payload shards")
+    b = ShardBuffers()
+    b.n = count
+    b.k = len(payloads)
+    b.theta = _cuda_contig(theta, torch.float32, count, "theta")
+    b.momentum = _cuda_contig(momentum, torch.float32, count, "momentum")
+    for i, p in enumerate(payloads):
+        b.payloads[i] = _cuda_contig(p, torch.bfloat16, count, "payload")
+    mp = _cuda_contig(mean_bf16, torch.bfloat16, count, "mean_bf16") if mean_bf16 is not None else None
+    out = C.c_double() if sq_mean else None
+    _check(lib().autoloco_shard_step(ctx.handle, C.byref(b), C.byref(coeffs), mp,
+                                     C.byref(out) if out is not None else None), "autoloco_shard_step", ctx)
+    return out.value if out is not None else None
 
 
 def autoloco_broadcast_reset(ctx: Context, theta, replicas, n=None) -> None:

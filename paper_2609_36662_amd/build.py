@@ -61,6 +61,7 @@ def jobs():
                 cmds.append([hipcc, *HIP_FLAGS, f"-DAL_RT={rt}", f"-DAL_RTNAME={rtname}", f"-DAL_STATS={st}",
                              f"-DAL_RESET={rs}", "-c", os.path.join(CSRC, "int8_inst.hip"), "-o", obj])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "adamw_inst.hip"), "-o", os.path.join(BUILD, "adamw.o")])
+    cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "shard_inst.hip"), "-o", os.path.join(BUILD, "shard.o")])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "api.hip"), "-o", os.path.join(BUILD, "api.o")])
     for src in ("scalar.cpp", "controller.cpp"):
         cmds.append(["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, src),

@@ -12,6 +12,7 @@
 
 #include "autoloco.h"
 #include "adamw_kernels.hpp"
+#include "shard_kernels.hpp"
 #include "int8_kernels.hpp"
 #include "round_kernels.hpp"
 
@@ -267,6 +268,51 @@ void finish_adamw(const double* sums, int k, double max_norm, autoloco_adamw_sta
         fin = fin && std::isfinite(out->grad_norm[i]);
     }
     out->finite = fin ? 1 : 0;
+}
+
+
+// Checks alignment and pairwise overlap of a list of ranges.
+int check_ranges(autoloco_ctx* ctx, const std::vector<Range>& r) {
+    for (const Range& x : r) {
+        if (x.lo == 0) return fail(ctx, AUTOLOCO_E_INVALID, std::string("null ") + x.name);
+        if (x.lo % 16 != 0) return fail(ctx, AUTOLOCO_E_ALIGN, std::string(x.name) + " not 16-byte aligned");
+    }
+    for (size_t i = 0; i < r.size(); ++i)
+        for (size_t j = i + 1; j < r.size(); ++j)
+            if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
+                return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    return AUTOLOCO_OK;
+}
+
+// Launches a kernel that leaves one float64 sum in ctx->sums; with out, waits
+// for it and stores it.
+template <typename Launch>
+int run_one_sum(autoloco_ctx* c, Launch launch, double* out) {
+    hipError_t e;
+    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    if ((e = launch()) != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if (c->timing) {
+        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+        c->timed_valid = true;
+        c->adamw_timed = false;
+    }
+    if (out != nullptr) {
+        if ((e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double), hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
+            return hip_fail(c, e, "hipMemcpyAsync");
+        if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        *out = c->host_sums[0];
+    }
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+// Workgroups of a kernel streaming 8 parameters per lane: three per CU at most.
+int blocks8(const autoloco_ctx* ctx, int64_t n) {
+    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * 3;
+    if (limit > kMaxBlocks) limit = kMaxBlocks;
+    int64_t want = (n / 8 + kBlock - 1) / kBlock;
+    if (want < 1) want = 1;
+    return static_cast<int>(want < limit ? want : limit);
 }
 
 void zero_stats(int k, double eps, autoloco_stats* out) {
@@ -622,6 +668,83 @@ int autoloco_free(autoloco_ctx* c, void* ptr) {
     const hipError_t e = hipFree(ptr);
     if (e != hipSuccess) return hip_fail(c, e, "hipFree");
     return AUTOLOCO_OK;
+}
+
+int autoloco_rank_payload(autoloco_ctx* c, int64_t n, const float* theta, const void* replica, int32_t dtype,
+                          uint16_t* payload, double* sq_norm) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (dtype != AUTOLOCO_F32 && dtype != AUTOLOCO_BF16) return fail(c, AUTOLOCO_E_INVALID, "unknown replica dtype");
+    if (n == 0) {
+        if (sq_norm != nullptr) *sq_norm = 0.0;
+        return AUTOLOCO_OK;
+    }
+    const uintptr_t un = static_cast<uintptr_t>(n);
+    std::vector<Range> r = {{reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(theta) + 4 * un, "theta"},
+                            {reinterpret_cast<uintptr_t>(replica),
+                             reinterpret_cast<uintptr_t>(replica) + un * replica_size(dtype), "replica"},
+                            {reinterpret_cast<uintptr_t>(payload), reinterpret_cast<uintptr_t>(payload) + 2 * un,
+                             "payload"}};
+    int st = check_ranges(c, r);
+    if (st != AUTOLOCO_OK) return st;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RankPayloadArgs a;
+    a.theta = theta;
+    a.replica = replica;
+    a.payload = payload;
+    a.n = n;
+    a.partials = c->partials;
+    a.ticket = c->ticket;
+    a.sums = c->sums;
+    const int blocks = blocks8(c, n);
+    const int rt = dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32;
+    return run_one_sum(c, [&] { return launch_rank_payload(rt, blocks, c->stream, a); }, sq_norm);
+}
+
+int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const autoloco_outer_coeffs* co,
+                        uint16_t* mean_bf16, double* sq_mean) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (b == nullptr || co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null buffers or coefficients");
+    if (b->n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(c, AUTOLOCO_E_INVALID, "k outside 1..16");
+    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
+        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    if (b->n == 0) {
+        if (sq_mean != nullptr) *sq_mean = 0.0;
+        return AUTOLOCO_OK;
+    }
+    const uintptr_t un = static_cast<uintptr_t>(b->n);
+    std::vector<Range> r = {
+        {reinterpret_cast<uintptr_t>(b->theta), reinterpret_cast<uintptr_t>(b->theta) + 4 * un, "theta"},
+        {reinterpret_cast<uintptr_t>(b->momentum), reinterpret_cast<uintptr_t>(b->momentum) + 4 * un, "momentum"}};
+    for (int k = 0; k < b->k; ++k)
+        r.push_back({reinterpret_cast<uintptr_t>(b->payloads[k]), reinterpret_cast<uintptr_t>(b->payloads[k]) + 2 * un,
+                     "payload"});
+    if (mean_bf16 != nullptr)
+        r.push_back({reinterpret_cast<uintptr_t>(mean_bf16), reinterpret_cast<uintptr_t>(mean_bf16) + 2 * un,
+                     "mean_bf16"});
+    int st = check_ranges(c, r);
+    if (st != AUTOLOCO_OK) return st;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    ShardArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.theta = b->theta;
+    a.momentum = b->momentum;
+    for (int k = 0; k < b->k; ++k) a.payloads[k] = b->payloads[k];
+    a.mean_out = mean_bf16;
+    a.n = b->n;
+    a.mu = static_cast<float>(co->mu);
+    a.eta = static_cast<float>(co->eta_out);
+    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    a.inv_k64 = 1.0 / static_cast<double>(b->k);
+    a.partials = c->partials;
+    a.ticket = c->ticket;
+    a.sums = c->sums;
+    const int blocks = blocks8(c, b->n);
+    const int k = b->k;
+    return run_one_sum(c, [&] { return launch_shard_step(k, blocks, c->stream, a); }, sq_mean);
 }
 
 int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const autoloco_adamw_coeffs* co,
