@@ -315,6 +315,117 @@ def bench_inner(args) -> int:
     return 0
 
 
+SHARE_METRIC = "per-GPU share of a one-replica-per-GPU round (BF16 payloads) params/s, 1.1B params K=8 GPUs"
+SHARE_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "shard_inst.hip", "round_kernels.hpp",
+                                                  "reduce.hpp")]
+
+
+def bench_share(args) -> int:
+    """GPU 0 of K: its worker's payload over the whole model, the step of its
+    1/K shard from K received payload shards, and its replica's reset.  The
+    all-to-all and all-gather between them are not run (one GPU)."""
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift, shapes
+
+    shape_name, k, rdt = WORKLOADS[args.workload][0], WORKLOADS[args.workload][1], WORKLOADS[args.workload][2]
+    if args.k:
+        k = args.k
+    n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
+    s_r = 4 if rdt == "f32" else 2
+    step8 = -(-(-(-n // k)) // 8) * 8
+    ns = min(n, step8)                                    # shard of GPU 0
+    b_payload, b_shard, b_reset = n * (4 + s_r + 2), ns * (16 + 2 * k), n * (4 + s_r)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sched = al.make_schedule()
+    coeffs = al.autoloco_outer_correction(al.make_outer_cfg(), al.autoloco_lr_mass(sched, 20_000, 750),
+                                          al.autoloco_lr_mass(sched, 20_000, 500))
+    log(f"per-GPU share {args.workload}: n={n:,} K={k} GPUs, shard {ns:,}; bytes payload "
+        f"{b_payload / 1e9:.2f} GB, shard step {b_shard / 1e9:.2f} GB, reset {b_reset / 1e9:.2f} GB")
+    ctx = al.autoloco_create(0)
+    # every buffer from the placement-aware allocator (shard buffers as views of full-size ones)
+    ts, spread = al.spread_tensors(ctx, n, [torch.float32, tdtype, torch.bfloat16, torch.float32]
+                                   + [torch.bfloat16] * (k + 1))
+    theta, rep, payload = ts[0], ts[1], ts[2]
+    v_shard = ts[3][:ns]
+    recv = [t[:ns] for t in ts[4:4 + k]]
+    mean = ts[4 + k][:ns]
+    inp = drift.RoundInputs(theta, torch.empty(0, device=dev), [rep])
+    drift._normal_into(theta, 0.02, 42, drift.ROLE_THETA, 0)
+    drift.fill_replicas(inp, seed=42)
+    drift._normal_into(v_shard, 1e-4, 42, drift.ROLE_MOMENTUM, 0)
+    for w in range(k):                                  # stand-ins for the workers' payload shards
+        x = torch.empty(ns, dtype=torch.float32, device=dev)
+        drift._normal_into(x, 1e-3, 100 + w, drift.ROLE_INDEP, w)
+        recv[w].copy_(x)
+        del x
+    torch.cuda.synchronize()
+    if args.grid:
+        al.autoloco_set_grid_limit(ctx, args.grid)
+    al.autoloco_set_timing(ctx, True)
+
+    def one_step():
+        al.autoloco_rank_payload(ctx, theta, rep, payload)
+        t_p = al.autoloco_last_kernel_ms(ctx)
+        al.autoloco_shard_step(ctx, theta[:ns], v_shard, recv, coeffs, mean_bf16=mean)
+        t_s = al.autoloco_last_kernel_ms(ctx)
+        al.autoloco_broadcast_reset(ctx, theta, [rep])
+        t_r = al.autoloco_last_kernel_ms(ctx)
+        return t_p, t_s, t_r
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    times = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        times.append(one_step())
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    tp, tsh, tr = (statistics.mean(t[i] for t in times) for i in range(3))
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step wall; payload {tp:.3f} ms "
+        f"({b_payload / tp / 1e6:.0f} GB/s), shard step {tsh:.3f} ms ({b_shard / tsh / 1e6:.0f} GB/s), "
+        f"reset {tr:.3f} ms ({b_reset / tr / 1e6:.0f} GB/s)")
+    achieved = b_payload / (tp * 1e-3) / 1e9
+    out = {
+        "metric": SHARE_METRIC,
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if rdt == "f32" else "f32 (bf16 replicas)",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: GPU 0 of K={k} (one worker replica per GPU), {n:,} parameters, "
+                        f"{rdt} replica, BF16 payloads; shard of {ns:,} parameters; collectives not run",
+            "n_params": n, "k": k, "shard": ns, "bytes": {"payload": b_payload, "shard_step": b_shard,
+                                                          "reset": b_reset},
+            "alloc": "spread" if spread else "spread (not spread)",
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "rank_payload_kernel",
+        },
+        "kernel_ms": {"payload": tp, "shard_step": tsh, "reset": tr},
+        "kernel_gbs": {"payload": b_payload / tp / 1e6, "shard_step": b_shard / tsh / 1e6,
+                       "reset": b_reset / tr / 1e6},
+        "cpu_baseline": None,
+        "kernel_source_sha256_16": kernel_source_hash(SHARE_SOURCES),
+    }
+    print(json.dumps(out), flush=True)
+    del ts, theta, rep, inp, recv, payload, v_shard, mean
+    ctx.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -335,8 +446,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
     ap.add_argument("--perturbed", type=int, default=3, help="extra rounds on freshly drawn replicas")
-    ap.add_argument("--step", choices=("round", "inner"), default="round",
-                    help="round: the synchronisation round; inner: one AdamW step of every worker")
+    ap.add_argument("--step", choices=("round", "inner", "share"), default="round",
+                    help="round: the synchronisation round; inner: one AdamW step of every worker; share: one "
+                         "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives)")
     ap.add_argument("--copy", action="store_true", help="inner: also write each worker's BF16 compute copy")
     args = ap.parse_args()
 
@@ -347,6 +459,8 @@ def main() -> int:
 
     if args.step == "inner":
         return bench_inner(args)
+    if args.step == "share":
+        return bench_share(args)
 
     import torch
     import paper_2609_36662_amd as al
