@@ -106,12 +106,30 @@ constexpr int kInt8Threads = 512;  // one codec block of 4,096 parameters per wo
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Each thread of a workgroup owns 8 parameters of the block (see the loop).
+template <bool B>
+struct BoolC {
+    static constexpr bool value = B;
+};
+
+// Each thread of a workgroup owns 8 parameters of a codec block.  fp32
+// replicas: two runs of 4 parameters, 2,048 apart (each wavefront instruction
+// covers 1 KB); bf16 replicas: one run of 8 (16 B of each replica per lane, as
+// the plain round loads them).  The loop runs over the full blocks, in which
+// every load and store is a whole vector; the one shorter last block, if any,
+// goes through a second instance of the same body with per-element accesses.
+// Up to 8 bf16 workers, the raw replica words and theta of a workgroup's next
+// block are loaded while the current one is encoded (the block barriers wait
+// for LDS traffic only), and pseudo-gradients are formed from the raw words
+// where they are used, which leaves the registers for it.
 template <int K, int RT, bool STATS, bool RESET>
 __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr int NT = kInt8Threads;
     constexpr int V = 8;
     constexpr int NS = STATS ? 2 * K + 1 : 1;
+    constexpr int G = RT == RT_F32 ? 2 : 1;
+    constexpr int W = V / G;
+    constexpr bool PF = RT == RT_BF16 && K <= 8;
+    constexpr int KW = RT == RT_BF16 ? K : 1;   // raw bf16 replica words held per thread
     __shared__ uint32_t lds_max[NT / 64 * K];   // worker block maxima
     __shared__ uint32_t lds_mmax[NT / 64];      // the mean's block maximum
 
@@ -119,75 +137,123 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
     for (int j = 0; j < NS; ++j) acc[j] = 0.0;
 
+    const int64_t nfull = a.n / kCodecBlock;
     const int64_t nblocks = (a.n + kCodecBlock - 1) / kCodecBlock;
-    for (int64_t blk = blockIdx.x; blk < nblocks; blk += gridDim.x) {
-        // fp32 replicas: two runs of 4 parameters, 2,048 apart (each wavefront
-        // instruction covers 1 KB); bf16 replicas: one run of 8 parameters (16 B
-        // of each replica per lane, as the plain round loads them)
-        constexpr int G = RT == RT_F32 ? 2 : 1;
-        constexpr int W = V / G;
+
+    // bf16: raw words and theta of one block (full: vector loads; else per element, zero beyond n)
+    u32x4 cw[KW];
+    float cth[V];
+    auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
+        const int64_t o = b * kCodecBlock + (int64_t)threadIdx.x * V;
+        if constexpr (FULL) {
+            const f32x4 t0 = ld_f4(a.theta + o), t1 = ld_f4(a.theta + o + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                t[e] = t0[e];
+                t[4 + e] = t1[e];
+            }
+#pragma unroll
+            for (int k = 0; k < KW; ++k) w[k] = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + o);
+        } else {
+            const int64_t left = a.n - o;
+#pragma unroll
+            for (int e = 0; e < V; ++e) t[e] = e < left ? a.theta[o + e] : 0.0f;
+#pragma unroll
+            for (int k = 0; k < KW; ++k) {
+                const uint16_t* r = static_cast<const uint16_t*>(a.replicas[k]) + o;
+                uint32_t h[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) h[e] = e < left ? r[e] : 0u;
+                w[k] = u32x4{h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16};
+            }
+        }
+    };
+
+    auto body = [&](int64_t blk, auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
         int64_t off[G];
         int valid[G];
         bool ok[V];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             off[g] = blk * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W;
-            const int64_t left = a.n - off[g];
-            valid[g] = left >= W ? W : (left > 0 ? (int)left : 0);
+            if constexpr (FULL) {
+                valid[g] = W;
+            } else {
+                const int64_t left = a.n - off[g];
+                valid[g] = left >= W ? W : (left > 0 ? (int)left : 0);
+            }
 #pragma unroll
             for (int e = 0; e < W; ++e) ok[g * W + e] = e < valid[g];
         }
 
-        float th[V], v[V], d[K][V];
+        float th[V], v[V], d[RT == RT_F32 ? K : 1][V];
+        u32x4 nw[PF ? K : 1];
+        float nth[V];
+        if constexpr (RT == RT_BF16) {
+            // momentum first: the update waits for it, and in-order completion
+            // then leaves the prefetch below in flight
+            const int64_t o = off[0];
+            if constexpr (FULL) {
+                const f32x4 v0 = ld_f4(a.momentum + o), v1 = ld_f4(a.momentum + o + 4);
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const int64_t o = off[g];
-            if (valid[g] == W) {
-#pragma unroll
-                for (int h = 0; h < W / 4; ++h) {
-                    const f32x4 t4 = ld_f4(a.theta + o + 4 * h), v4 = ld_f4(a.momentum + o + 4 * h);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        th[g * W + 4 * h + e] = t4[e];
-                        v[g * W + 4 * h + e] = v4[e];
-                    }
-                }
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    if constexpr (RT == RT_F32) {
-                        const f32x4 r4 = ld_f4(static_cast<const float*>(a.replicas[k]) + o);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) d[k][g * W + e] = th[g * W + e] - r4[e];
-                    } else {
-                        const u32x4 w = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + o);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            d[k][2 * e] = th[2 * e] - bf16_lo(w[e]);
-                            d[k][2 * e + 1] = th[2 * e + 1] - bf16_hi(w[e]);
-                        }
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    v[e] = v0[e];
+                    v[4 + e] = v1[e];
                 }
             } else {
 #pragma unroll
-                for (int e = 0; e < W; ++e) {
-                    const bool in = e < valid[g];
-                    const int x = g * W + e;
-                    th[x] = in ? a.theta[o + e] : 0.0f;
-                    v[x] = in ? a.momentum[o + e] : 0.0f;
+                for (int e = 0; e < V; ++e) v[e] = e < valid[0] ? a.momentum[o + e] : 0.0f;
+            }
+            if constexpr (PF && FULL) {
+                // next full block of this workgroup; on its last one, this block again
+                // (every iteration issues the same loads)
+                const int64_t nb = blk + gridDim.x < nfull ? blk + gridDim.x : blk;
+                load_bf16(nb, nw, nth, BoolC<true>{});
+            } else {
+                load_bf16(blk, cw, cth, full_c);
+            }
+#pragma unroll
+            for (int e = 0; e < V; ++e) th[e] = cth[e];
+        } else {
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const int64_t o = off[g];
+                if constexpr (FULL) {
+                    const f32x4 t4 = ld_f4(a.theta + o), v4 = ld_f4(a.momentum + o);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        th[g * W + e] = t4[e];
+                        v[g * W + e] = v4[e];
+                    }
 #pragma unroll
                     for (int k = 0; k < K; ++k) {
-                        float r = 0.0f;
-                        if (in) {
-                            if constexpr (RT == RT_F32)
-                                r = static_cast<const float*>(a.replicas[k])[o + e];
-                            else
-                                r = __uint_as_float((uint32_t) static_cast<const uint16_t*>(a.replicas[k])[o + e] << 16);
-                        }
-                        d[k][x] = in ? th[x] - r : 0.0f;
+                        const f32x4 r4 = ld_f4(static_cast<const float*>(a.replicas[k]) + o);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) d[k][g * W + e] = th[g * W + e] - r4[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < W; ++e) {
+                        const bool in = e < valid[g];
+                        const int x = g * W + e;
+                        th[x] = in ? a.theta[o + e] : 0.0f;
+                        v[x] = in ? a.momentum[o + e] : 0.0f;
+#pragma unroll
+                        for (int k = 0; k < K; ++k)
+                            d[k][x] = in ? th[x] - static_cast<const float*>(a.replicas[k])[o + e] : 0.0f;
                     }
                 }
             }
         }
+        // pseudo-gradient k of parameter e (bf16: from the raw replica word)
+        auto D = [&](int k, int e) -> float {
+            if constexpr (RT == RT_F32)
+                return d[k][e];
+            else
+                return th[e] - ((e & 1) ? bf16_hi(cw[k][e >> 1]) : bf16_lo(cw[k][e >> 1]));
+        };
 
         // local-drift energy before quantisation
         if constexpr (STATS) {
@@ -195,7 +261,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             for (int k = 0; k < K; ++k) {
                 float s = 0.f;
 #pragma unroll
-                for (int e = 0; e < V; ++e) s = __builtin_fmaf(d[k][e], d[k][e], s);
+                for (int e = 0; e < V; ++e) s = __builtin_fmaf(D(k, e), D(k, e), s);
                 acc[k] += (double)s;
             }
         }
@@ -206,7 +272,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         for (int k = 0; k < K; ++k) {
             float m = 0.f;
 #pragma unroll
-            for (int e = 0; e < V; ++e) m = fmaxf(m, fabsf(d[k][e]));
+            for (int e = 0; e < V; ++e) m = fmaxf(m, fabsf(D(k, e)));
             amax[k] = m;
         }
         block_max<K, NT>(amax, lds_max);
@@ -220,7 +286,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             const float s = codec_scale(amax[k]);
             const float r = 1.0f / s;
 #pragma unroll
-            for (int e = 0; e < V; ++e) sum[e] += (double)(codec_q(d[k][e], s, r) * s);
+            for (int e = 0; e < V; ++e) sum[e] += (double)(codec_q(D(k, e), s, r) * s);
         }
         float mean[V];
         float mmax[1] = {0.f};
@@ -242,7 +308,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         if (a.mean_codes != nullptr) {
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                if (valid[g] == W) {
+                if (FULL || valid[g] == W) {
                     uint32_t w[W / 4];
 #pragma unroll
                     for (int h = 0; h < W / 4; ++h) {
@@ -269,7 +335,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 float q = 0.f;
 #pragma unroll
                 for (int e = 0; e < V; ++e) {
-                    const float t = d[k][e] - agg[e];
+                    const float t = D(k, e) - agg[e];
                     q = __builtin_fmaf(t, t, q);
                 }
                 acc[K + k] += (double)q;
@@ -294,7 +360,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             const int64_t o = off[g];
             const float* tn = th_new + g * W;
             const float* vn = v_new + g * W;
-            if (valid[g] == W) {
+            if (FULL || valid[g] == W) {
 #pragma unroll
                 for (int h = 0; h < W / 4; ++h) {
                     st_f4(a.theta + o + 4 * h, f32x4{tn[4 * h], tn[4 * h + 1], tn[4 * h + 2], tn[4 * h + 3]});
@@ -331,7 +397,24 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 }
             }
         }
+        if constexpr (PF && FULL) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) cw[k] = nw[k];
+#pragma unroll
+            for (int e = 0; e < V; ++e) cth[e] = nth[e];
+        }
+    };
+
+    if constexpr (PF) {
+        if (blockIdx.x < nfull) load_bf16(blockIdx.x, cw, cth, BoolC<true>{});
+        // the first block's words are complete before the loop, as on every later
+        // entry (where they come from register moves), so the loop needs no wait
+        // for them
+        __builtin_amdgcn_s_waitcnt(0);
     }
+    for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{});
+    // the shorter last block belongs to the workgroup the grid stride gives it
+    if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{});
 
     if constexpr (STATS) grid_reduce<NS, NT>(acc, a.partials, a.ticket, a.sums);
 }
