@@ -390,6 +390,8 @@ def bench_share(args) -> int:
         f"({b_payload / tp / 1e6:.0f} GB/s), shard step {tsh:.3f} ms ({b_shard / tsh / 1e6:.0f} GB/s), "
         f"reset {tr:.3f} ms ({b_reset / tr / 1e6:.0f} GB/s)")
     achieved = b_payload / (tp * 1e-3) / 1e9
+    ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
+    traffic = committed_traffic(f"share_{rdt}_k{k}_{args.workload}", SHARE_SOURCES)
     out = {
         "metric": SHARE_METRIC,
         "value": n / (ms_per_step * 1e-3),
@@ -412,8 +414,9 @@ def bench_share(args) -> int:
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "rank_payload_kernel",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": "rank_payload_kernel",
         },
+        "copy_ceiling_gbs": ceiling,
         "kernel_ms": {"payload": tp, "shard_step": tsh, "reset": tr},
         "kernel_gbs": {"payload": b_payload / tp / 1e6, "shard_step": b_shard / tsh / 1e6,
                        "reset": b_reset / tr / 1e6},
