@@ -85,6 +85,12 @@ __device__ __forceinline__ u32x4 ld_u4_at(const void* base, uint32_t off) {
 __device__ __forceinline__ void st_u4_at(void* base, uint32_t off, u32x4 v) {
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(static_cast<char*>(base) + off));
 }
+__device__ __forceinline__ u32x2r ld_u2_at(const void* base, uint32_t off) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x2r*>(static_cast<const char*>(base) + off));
+}
+__device__ __forceinline__ void st_u2_at(void* base, uint32_t off, u32x2r v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x2r*>(static_cast<char*>(base) + off));
+}
 
 // bf16 <-> fp32.  Widening is exact; narrowing rounds to nearest, ties to
 // even, keeps infinities and turns every NaN into the quiet NaN 0x7FC0 with
@@ -154,69 +160,67 @@ __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K]
 // ------------------------------------------------------------ round kernel --
 template <int K, int RT, bool STATS, bool UPDATE, bool RESET, bool BF16P = false>
 __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
-    constexpr int V = RT == RT_F32 ? 4 : 8;  // parameters per 16-byte replica vector
     constexpr int NS = STATS ? 2 * K + 1 : 1;
     double acc[NS];
 #pragma unroll
     for (int j = 0; j < NS; ++j) acc[j] = 0.0;
 
-    const int64_t nvec = a.n / V;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    // Parameters in runs of 4 ("quads": 16 bytes of fp32, 8 of bf16).  The
+    // loop walks wave-uniform windows: each stream's window base stays in
+    // scalar registers and a lane adds only its 32-bit offset.  fp32 replicas:
+    // a lane owns one quad per window of 256; bf16 replicas: two, 256 quads
+    // apart (a window of 512), so every load and store instruction of a
+    // wavefront covers one contiguous run (1 KB of fp32, 512 B of bf16) and no
+    // cache line is written in parts.
+    constexpr int R = RT == RT_F32 ? 1 : 2;   // quads per lane per window
+    constexpr int V = 4 * R;                  // parameters per lane per window
+    const int64_t nq = a.n / 4;
+    const int64_t qstride = (int64_t)gridDim.x * kBlock * R;
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
 
-    // The loop walks wave-uniform windows of kBlock vectors: each stream's window
-    // base stays in scalar registers and a lane adds only its 32-bit offset.
-    for (int64_t vb = (int64_t)blockIdx.x * kBlock; vb < nvec; vb += stride) {
-        if (vb + threadIdx.x >= nvec) continue;
-        const int64_t wb = vb * V;                        // first parameter of the window
-        const uint32_t fo = threadIdx.x * (uint32_t)V * 4u; // this lane's byte offset in fp32 buffers
-        const uint32_t ro = threadIdx.x * 16u;             // and in replica buffers (16 bytes per lane)
+    for (int64_t qb = (int64_t)blockIdx.x * kBlock * R; qb < nq; qb += qstride) {
+        if (qb + threadIdx.x >= nq) continue;
+        // run 1 (bf16) exists unless this is the last, shorter window
+        const bool ok1 = R == 2 && qb + kBlock + threadIdx.x < nq;
+        const int64_t wb = qb * 4;                        // first parameter of the window
         float* const th_w = a.theta + wb;
         float* const mo_w = UPDATE ? a.momentum + wb : nullptr;
         float th[V], v[V], r[K][V];
-        if constexpr (RT == RT_F32) {
+#pragma unroll
+        for (int h = 0; h < R; ++h) {
+            const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;   // byte offset in fp32 buffers
+            if (h == 1 && !ok1) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    th[4 * h + e] = v[4 * h + e] = 0.f;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) r[k][4 * h + e] = 0.f;
+                }
+                continue;
+            }
             const f32x4 t4 = ld_f4_at(th_w, fo);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) th[e] = t4[e];
+            for (int e = 0; e < 4; ++e) th[4 * h + e] = t4[e];
             if constexpr (UPDATE) {
                 const f32x4 v4 = ld_f4_at(mo_w, fo);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = v4[e];
+                for (int e = 0; e < 4; ++e) v[4 * h + e] = v4[e];
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = 0.f;
+                for (int e = 0; e < 4; ++e) v[4 * h + e] = 0.f;
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                const f32x4 r4 = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, ro);
+                if constexpr (RT == RT_F32) {
+                    const f32x4 r4 = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, fo);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
-            }
-        } else {
-            const f32x4 t0 = ld_f4_at(th_w, fo), t1 = ld_f4_at(th_w, fo + 16u);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                th[e] = t0[e];
-                th[4 + e] = t1[e];
-            }
-            if constexpr (UPDATE) {
-                const f32x4 v0 = ld_f4_at(mo_w, fo), v1 = ld_f4_at(mo_w, fo + 16u);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    v[e] = v0[e];
-                    v[4 + e] = v1[e];
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[e] = 0.f;
-            }
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const u32x4 w = ld_u4_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, ro);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    r[k][2 * e] = bf16_lo(w[e]);
-                    r[k][2 * e + 1] = bf16_hi(w[e]);
+                    for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
+                } else {
+                    const u32x2r w = ld_u2_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, fo / 2);
+                    r[k][4 * h] = bf16_lo(w[0]);
+                    r[k][4 * h + 1] = bf16_hi(w[0]);
+                    r[k][4 * h + 2] = bf16_lo(w[1]);
+                    r[k][4 * h + 3] = bf16_hi(w[1]);
                 }
             }
         }
@@ -233,20 +237,6 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
             for (int k = 0; k < K; ++k) re[k] = r[k][e];
             one_param<K, STATS, UPDATE, BF16P>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e], pb[e]);
         }
-        if constexpr (BF16P) {
-            if (a.payload != nullptr) {
-                // 2 bytes per parameter: 8 (fp32 replicas) or 16 bytes per lane
-                char* const pw = reinterpret_cast<char*>(a.payload + wb);
-                const uint32_t po = threadIdx.x * (uint32_t)V * 2u;
-                if constexpr (V == 4)
-                    __builtin_nontemporal_store(u32x2r{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16},
-                                                reinterpret_cast<u32x2r*>(pw + po));
-                else
-                    __builtin_nontemporal_store(u32x4{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16, pb[4] | pb[5] << 16,
-                                                      pb[6] | pb[7] << 16},
-                                                reinterpret_cast<u32x4*>(pw + po));
-            }
-        }
         if constexpr (STATS) {
 #pragma unroll
             for (int k = 0; k < K; ++k) {
@@ -255,32 +245,36 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
             }
             acc[2 * K] += (double)m;
         }
-        if constexpr (UPDATE) {
-            if constexpr (RT == RT_F32) {
-                st_f4_at(th_w, fo, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-                st_f4_at(mo_w, fo, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
-                if constexpr (RESET) {
-                    const f32x4 o = {th_new[0], th_new[1], th_new[2], th_new[3]};
 #pragma unroll
-                    for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, ro, o);
-                }
-            } else {
-                st_f4_at(th_w, fo, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-                st_f4_at(th_w, fo + 16u, f32x4{th_new[4], th_new[5], th_new[6], th_new[7]});
-                st_f4_at(mo_w, fo, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
-                st_f4_at(mo_w, fo + 16u, f32x4{v_new[4], v_new[5], v_new[6], v_new[7]});
+        for (int h = 0; h < R; ++h) {
+            if (h == 1 && !ok1) continue;
+            const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;
+            if constexpr (BF16P) {
+                // 2 bytes per parameter: 8 per quad
+                if (a.payload != nullptr)
+                    st_u2_at(a.payload + wb, fo / 2, u32x2r{pb[4 * h] | pb[4 * h + 1] << 16,
+                                                            pb[4 * h + 2] | pb[4 * h + 3] << 16});
+            }
+            if constexpr (UPDATE) {
+                const f32x4 o = {th_new[4 * h], th_new[4 * h + 1], th_new[4 * h + 2], th_new[4 * h + 3]};
+                st_f4_at(th_w, fo, o);
+                st_f4_at(mo_w, fo, f32x4{v_new[4 * h], v_new[4 * h + 1], v_new[4 * h + 2], v_new[4 * h + 3]});
                 if constexpr (RESET) {
-                    const u32x4 o = {bf16_pack(th_new[0], th_new[1]), bf16_pack(th_new[2], th_new[3]),
-                                     bf16_pack(th_new[4], th_new[5]), bf16_pack(th_new[6], th_new[7])};
+                    if constexpr (RT == RT_F32) {
 #pragma unroll
-                    for (int k = 0; k < K; ++k) st_u4_at(static_cast<uint16_t*>(a.replicas[k]) + wb, ro, o);
+                        for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, fo, o);
+                    } else {
+                        const u32x2r w = {bf16_pack(o[0], o[1]), bf16_pack(o[2], o[3])};
+#pragma unroll
+                        for (int k = 0; k < K; ++k) st_u2_at(static_cast<uint16_t*>(a.replicas[k]) + wb, fo / 2, w);
+                    }
                 }
             }
         }
     }
 
-    // Ragged tail: the last n mod V parameters, one per thread of workgroup 0.
-    const int64_t tail0 = nvec * V;
+    // Ragged tail: the last n mod 4 parameters, one per thread of workgroup 0.
+    const int64_t tail0 = nq * 4;
     if (gtid < a.n - tail0) {
         const int64_t j = tail0 + gtid;
         const float th = a.theta[j];
