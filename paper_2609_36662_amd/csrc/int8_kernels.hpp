@@ -111,10 +111,9 @@ struct BoolC {
     static constexpr bool value = B;
 };
 
-// Each thread of a workgroup owns 8 parameters of a codec block.  fp32
-// replicas: two runs of 4 parameters, 2,048 apart (each wavefront instruction
-// covers 1 KB); bf16 replicas: one run of 8 (16 B of each replica per lane, as
-// the plain round loads them).  The loop runs over the full blocks, in which
+// Each thread of a workgroup owns 8 parameters of a codec block: two runs of
+// 4, 2,048 apart, so every wavefront instruction covers one contiguous run
+// (1 KB of fp32, 512 B of bf16) and no cache line is written in parts.  The loop runs over the full blocks, in which
 // every load and store is a whole vector; the one shorter last block, if any,
 // goes through a second instance of the same body with per-element accesses.
 // Up to 8 bf16 workers, the raw replica words and theta of a workgroup's next
@@ -126,7 +125,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr int NT = kInt8Threads;
     constexpr int V = 8;
     constexpr int NS = STATS ? 2 * K + 1 : 1;
-    constexpr int G = RT == RT_F32 ? 2 : 1;
+    constexpr int G = 2;   // runs of W parameters per thread
     constexpr int W = V / G;
     constexpr bool PF = RT == RT_BF16 && K <= 8;
     constexpr int KW = RT == RT_BF16 ? K : 1;   // raw bf16 replica words held per thread
@@ -140,32 +139,35 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     const int64_t nfull = a.n / kCodecBlock;
     const int64_t nblocks = (a.n + kCodecBlock - 1) / kCodecBlock;
 
-    // bf16: raw words and theta of one block (full: vector loads; else per element, zero beyond n)
-    u32x4 cw[KW];
+    // bf16: raw words (two per run) and theta of one block (full: vector loads;
+    // else per element, zero beyond n)
+    u32x2 cw[KW][G];
     float cth[V];
     auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto full_c) {
         constexpr bool FULL = decltype(full_c)::value;
-        const int64_t o = b * kCodecBlock + (int64_t)threadIdx.x * V;
-        if constexpr (FULL) {
-            const f32x4 t0 = ld_f4(a.theta + o), t1 = ld_f4(a.theta + o + 4);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                t[e] = t0[e];
-                t[4 + e] = t1[e];
-            }
+        for (int g = 0; g < G; ++g) {
+            const int64_t o = b * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W;
+            if constexpr (FULL) {
+                const f32x4 t4 = ld_f4(a.theta + o);
 #pragma unroll
-            for (int k = 0; k < KW; ++k) w[k] = ld_u4(static_cast<const uint16_t*>(a.replicas[k]) + o);
-        } else {
-            const int64_t left = a.n - o;
+                for (int e = 0; e < W; ++e) t[g * W + e] = t4[e];
 #pragma unroll
-            for (int e = 0; e < V; ++e) t[e] = e < left ? a.theta[o + e] : 0.0f;
+                for (int k = 0; k < KW; ++k)
+                    w[k][g] = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x2*>(static_cast<const uint16_t*>(a.replicas[k]) + o));
+            } else {
+                const int64_t left = a.n - o;
 #pragma unroll
-            for (int k = 0; k < KW; ++k) {
-                const uint16_t* r = static_cast<const uint16_t*>(a.replicas[k]) + o;
-                uint32_t h[V];
+                for (int e = 0; e < W; ++e) t[g * W + e] = e < left ? a.theta[o + e] : 0.0f;
 #pragma unroll
-                for (int e = 0; e < V; ++e) h[e] = e < left ? r[e] : 0u;
-                w[k] = u32x4{h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16};
+                for (int k = 0; k < KW; ++k) {
+                    const uint16_t* r = static_cast<const uint16_t*>(a.replicas[k]) + o;
+                    uint32_t h[W];
+#pragma unroll
+                    for (int e = 0; e < W; ++e) h[e] = e < left ? r[e] : 0u;
+                    w[k][g] = u32x2{h[0] | h[1] << 16, h[2] | h[3] << 16};
+                }
             }
         }
     };
@@ -189,22 +191,22 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
 
         float th[V], v[V], d[RT == RT_F32 ? K : 1][V];
-        u32x4 nw[PF ? K : 1];
+        u32x2 nw[PF ? K : 1][G];
         float nth[V];
         if constexpr (RT == RT_BF16) {
             // momentum first: the update waits for it, and in-order completion
             // then leaves the prefetch below in flight
-            const int64_t o = off[0];
-            if constexpr (FULL) {
-                const f32x4 v0 = ld_f4(a.momentum + o), v1 = ld_f4(a.momentum + o + 4);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    v[e] = v0[e];
-                    v[4 + e] = v1[e];
+            for (int g = 0; g < G; ++g) {
+                const int64_t o = off[g];
+                if constexpr (FULL) {
+                    const f32x4 v4 = ld_f4(a.momentum + o);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) v[g * W + e] = v4[e];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < W; ++e) v[g * W + e] = e < valid[g] ? a.momentum[o + e] : 0.0f;
                 }
-            } else {
-#pragma unroll
-                for (int e = 0; e < V; ++e) v[e] = e < valid[0] ? a.momentum[o + e] : 0.0f;
             }
             if constexpr (PF && FULL) {
                 // next full block of this workgroup; on its last one, this block again
@@ -252,7 +254,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             if constexpr (RT == RT_F32)
                 return d[k][e];
             else
-                return th[e] - ((e & 1) ? bf16_hi(cw[k][e >> 1]) : bf16_lo(cw[k][e >> 1]));
+                return th[e] - ((e & 1) ? bf16_hi(cw[k][e / W][(e % W) >> 1]) : bf16_lo(cw[k][e / W][(e % W) >> 1]));
         };
 
         // local-drift energy before quantisation
@@ -372,10 +374,10 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
                         for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + o, t4);
                     } else {
-                        const u32x4 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3]), bf16_pack(tn[4], tn[5]),
-                                         bf16_pack(tn[6], tn[7])};
+                        const u32x2 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3])};
 #pragma unroll
-                        for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + o, w);
+                        for (int k = 0; k < K; ++k)
+                            __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.replicas[k]) + o));
                     }
                 }
             } else {
@@ -399,7 +401,10 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
         if constexpr (PF && FULL) {
 #pragma unroll
-            for (int k = 0; k < K; ++k) cw[k] = nw[k];
+            for (int k = 0; k < K; ++k) {
+                cw[k][0] = nw[k][0];
+                cw[k][1] = nw[k][1];
+            }
 #pragma unroll
             for (int e = 0; e < V; ++e) cth[e] = nth[e];
         }
