@@ -306,9 +306,9 @@ int run_one_sum(autoloco_ctx* c, Launch launch, double* out) {
     return AUTOLOCO_OK;
 }
 
-// Workgroups of the per-GPU share kernels (8 parameters per lane): two per CU
-// at most (measured at 1.1B / 8 shards on MI355X: 512 workgroups 7-9 % faster
-// than 768, 2,048 and more 15-90 % slower).
+// Workgroups of the per-GPU share kernels (two quads of 4 parameters per lane
+// per window): two per CU at most (measured at 1.1B / 8 shards on MI355X: 512
+// workgroups 7-9 % faster than 768, 2,048 and more 15-90 % slower).
 int blocks8(const autoloco_ctx* ctx, int64_t n) {
     int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * 2;
     if (limit > kMaxBlocks) limit = kMaxBlocks;

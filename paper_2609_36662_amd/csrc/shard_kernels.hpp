@@ -12,8 +12,7 @@
 //       mean = bf16(fp32(sum_k payload_k (float64, worker order) * 1/K))
 //       M_s = sum mean^2; v' = mu v + mean*scale; theta' = theta - eta (mean*scale + mu v')
 //
-// Both stream 16-byte vectors (8 parameters per lane) and reduce their one sum
-// with the deterministic two-stage reduction.
+// Both reduce their one sum with the deterministic two-stage reduction.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -47,45 +46,49 @@ struct ShardArgs {
     double* sums;
 };
 
+// Both kernels walk runs of 4 parameters ("quads"); a lane owns two quads per
+// window of 512, 256 quads apart, so every wavefront instruction covers one
+// contiguous run (1 KB of fp32, 512 B of bf16) and no cache line is written in
+// parts.  The last n mod 4 parameters go to threads of workgroup 0.
 template <int RT>
 __global__ void __launch_bounds__(kBlock) rank_payload_kernel(RankPayloadArgs a) {
     double acc[1] = {0.0};
-    const int64_t nvec = a.n / 8;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < nvec; i += stride) {
-        const int64_t o = 8 * i;
-        const f32x4 t0 = ld_f4(a.theta + o), t1 = ld_f4(a.theta + o + 4);
-        float r[8];
-        if constexpr (RT == RT_F32) {
-            const f32x4 r0 = ld_f4(static_cast<const float*>(a.replica) + o);
-            const f32x4 r1 = ld_f4(static_cast<const float*>(a.replica) + o + 4);
+    const int64_t nq = a.n / 4;
+    const int64_t stride = (int64_t)gridDim.x * kBlock * 2;
+    for (int64_t qb = (int64_t)blockIdx.x * kBlock * 2; qb < nq; qb += stride) {
+        float s = 0.f;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int64_t q = qb + h * kBlock + threadIdx.x;
+            if (q >= nq) break;
+            const int64_t o = 4 * q;
+            const f32x4 t = ld_f4(a.theta + o);
+            float r[4];
+            if constexpr (RT == RT_F32) {
+                const f32x4 r4 = ld_f4(static_cast<const float*>(a.replica) + o);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r[e] = r4[e];
+            } else {
+                const u32x2r w = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x2r*>(static_cast<const uint16_t*>(a.replica) + o));
+                r[0] = bf16_lo(w[0]);
+                r[1] = bf16_hi(w[0]);
+                r[2] = bf16_lo(w[1]);
+                r[3] = bf16_hi(w[1]);
+            }
+            float d[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                r[e] = r0[e];
-                r[4 + e] = r1[e];
+                d[e] = t[e] - r[e];
+                s = __builtin_fmaf(d[e], d[e], s);
             }
-        } else {
-            const u32x4 w = ld_u4(static_cast<const uint16_t*>(a.replica) + o);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                r[2 * e] = bf16_lo(w[e]);
-                r[2 * e + 1] = bf16_hi(w[e]);
-            }
+            __builtin_nontemporal_store(u32x2r{bf16_pack(d[0], d[1]), bf16_pack(d[2], d[3])},
+                                        reinterpret_cast<u32x2r*>(a.payload + o));
         }
-        float d[8], s = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            d[e] = t0[e] - r[e];
-            d[4 + e] = t1[e] - r[4 + e];
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s = __builtin_fmaf(d[e], d[e], s);
         acc[0] += (double)s;
-        st_u4(a.payload + o, u32x4{bf16_pack(d[0], d[1]), bf16_pack(d[2], d[3]), bf16_pack(d[4], d[5]),
-                                   bf16_pack(d[6], d[7])});
     }
-    if (blockIdx.x == 0 && threadIdx.x < (a.n & 7)) {
-        const int64_t j = nvec * 8 + threadIdx.x;
+    if (blockIdx.x == 0 && threadIdx.x < (a.n & 3)) {
+        const int64_t j = nq * 4 + threadIdx.x;
         float r;
         if constexpr (RT == RT_F32)
             r = static_cast<const float*>(a.replica)[j];
@@ -117,50 +120,45 @@ __device__ __forceinline__ float shard_one(const ShardArgs& a, const float (&b)[
 template <int K>
 __global__ void __launch_bounds__(kBlock) shard_step_kernel(ShardArgs a) {
     double acc[1] = {0.0};
-    const int64_t nvec = a.n / 8;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < nvec; i += stride) {
-        const int64_t o = 8 * i;
-        const f32x4 t0 = ld_f4(a.theta + o), t1 = ld_f4(a.theta + o + 4);
-        const f32x4 v0 = ld_f4(a.momentum + o), v1 = ld_f4(a.momentum + o + 4);
-        float b[K][8];
+    const int64_t nq = a.n / 4;
+    const int64_t stride = (int64_t)gridDim.x * kBlock * 2;
+    for (int64_t qb = (int64_t)blockIdx.x * kBlock * 2; qb < nq; qb += stride) {
+        float m = 0.f;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const u32x4 w = ld_u4(a.payloads[k] + o);
+        for (int h = 0; h < 2; ++h) {
+            const int64_t q = qb + h * kBlock + threadIdx.x;
+            if (q >= nq) break;
+            const int64_t o = 4 * q;
+            const f32x4 t4 = ld_f4(a.theta + o), v4 = ld_f4(a.momentum + o);
+            float b[K][4];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const u32x2r w = __builtin_nontemporal_load(reinterpret_cast<const u32x2r*>(a.payloads[k] + o));
+                b[k][0] = bf16_lo(w[0]);
+                b[k][1] = bf16_hi(w[0]);
+                b[k][2] = bf16_lo(w[1]);
+                b[k][3] = bf16_hi(w[1]);
+            }
+            float th_new[4], v_new[4];
+            uint32_t pb[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                b[k][2 * e] = bf16_lo(w[e]);
-                b[k][2 * e + 1] = bf16_hi(w[e]);
+                float be[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) be[k] = b[k][e];
+                const float mean = shard_one<K>(a, be, t4[e], v4[e], th_new[e], v_new[e], pb[e]);
+                m = __builtin_fmaf(mean, mean, m);
             }
-        }
-        float th[8], v[8], th_new[8], v_new[8], m = 0.f;
-        uint32_t pb[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            th[e] = t0[e];
-            th[4 + e] = t1[e];
-            v[e] = v0[e];
-            v[4 + e] = v1[e];
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float be[K];
-#pragma unroll
-            for (int k = 0; k < K; ++k) be[k] = b[k][e];
-            const float mean = shard_one<K>(a, be, th[e], v[e], th_new[e], v_new[e], pb[e]);
-            m = __builtin_fmaf(mean, mean, m);
+            st_f4(a.theta + o, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+            st_f4(a.momentum + o, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+            if (a.mean_out != nullptr)
+                __builtin_nontemporal_store(u32x2r{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16},
+                                            reinterpret_cast<u32x2r*>(a.mean_out + o));
         }
         acc[0] += (double)m;
-        st_f4(a.theta + o, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-        st_f4(a.theta + o + 4, f32x4{th_new[4], th_new[5], th_new[6], th_new[7]});
-        st_f4(a.momentum + o, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
-        st_f4(a.momentum + o + 4, f32x4{v_new[4], v_new[5], v_new[6], v_new[7]});
-        if (a.mean_out != nullptr)
-            st_u4(a.mean_out + o, u32x4{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16, pb[4] | pb[5] << 16,
-                                        pb[6] | pb[7] << 16});
     }
-    if (blockIdx.x == 0 && threadIdx.x < (a.n & 7)) {
-        const int64_t j = nvec * 8 + threadIdx.x;
+    if (blockIdx.x == 0 && threadIdx.x < (a.n & 3)) {
+        const int64_t j = nq * 4 + threadIdx.x;
         float be[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) be[k] = __uint_as_float((uint32_t)a.payloads[k][j] << 16);

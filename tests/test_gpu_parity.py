@@ -83,7 +83,7 @@ def test_every_worker_count_bf16(ctx, k):
     _check_full_round(ctx, 65_539, k, replica_dtype=torch.bfloat16, seed=200 + k, normalize=k % 2 == 1)
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 9, 255, 1023, 1025, 262_147, 2_097_155])
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 9, 255, 1023, 1025, 5000, 7579, 262_147, 2_097_155])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_ragged_sizes(ctx, n, dtype):
     _check_full_round(ctx, n, 3, replica_dtype=dtype, seed=n % 97)
