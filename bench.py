@@ -448,7 +448,8 @@ def main() -> int:
     ap.add_argument("--cpu-sample", type=int, default=1 << 22)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
-    ap.add_argument("--perturbed", type=int, default=3, help="extra rounds on freshly drawn replicas")
+    ap.add_argument("--perturbed", type=int, default=20,
+                    help="extra rounds, each on freshly drawn replicas (drawn outside the timing)")
     ap.add_argument("--step", choices=("round", "inner", "share"), default="round",
                     help="round: the synchronisation round; inner: one AdamW step of every worker; share: one "
                          "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives)")
@@ -557,14 +558,17 @@ def main() -> int:
     log(f"timed {args.steps} rounds: {ms_per_step:.3f} ms/round wall, kernel mean "
         f"{statistics.mean(kernel_ms):.3f} ms")
 
-    perturbed_ms = []
+    perturbed_ms, perturbed_wall = [], []
     for i in range(args.perturbed):
         drift.fill_replicas(inp, seed=1000 + i, recipe=recipe)
         torch.cuda.synchronize()
-        _, ms = one_round()
+        t1 = time.perf_counter()
+        _, ms = one_round()                      # blocks until the sums are on the host
+        perturbed_wall.append((time.perf_counter() - t1) * 1e3)
         perturbed_ms.append(ms)
     if perturbed_ms:
-        log(f"rounds on freshly drawn replicas: kernel {statistics.median(perturbed_ms):.3f} ms (median)")
+        log(f"{len(perturbed_ms)} rounds on freshly drawn replicas: kernel {statistics.median(perturbed_ms):.3f} ms, "
+            f"round {statistics.median(perturbed_wall):.3f} ms (medians)")
 
     ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
 
@@ -612,6 +616,8 @@ def main() -> int:
         "kernel_ms_mean": mean_ms,
         "kernel_ms_min": min(kernel_ms),
         "kernel_ms_perturbed_median": statistics.median(perturbed_ms) if perturbed_ms else None,
+        "round_ms_perturbed_median": statistics.median(perturbed_wall) if perturbed_wall else None,
+        "perturbed_rounds": len(perturbed_ms),
         "copy_ceiling_gbs": ceiling,
         "first_round_stats": {k2: first_stats[k2] for k2 in ("D", "C", "disagreement", "finite")}
         if first_stats else None,
