@@ -1,0 +1,23 @@
+"""bench.py's command line on the CPU: more than one GPU is refused with a
+message and exit status 2, before anything touches a device."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    for n in (2, 8):
+        p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", str(n)],
+                           capture_output=True, text=True, timeout=120)
+        assert p.returncode == 2
+        assert "one GPU" in p.stderr and p.stdout == ""
+
+
+def test_help_lists_the_modes():
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"], capture_output=True, text=True,
+                       timeout=120)
+    assert p.returncode == 0
+    for word in ("--codec", "--step", "--workload", "--steps", "--warmup"):
+        assert word in p.stdout
