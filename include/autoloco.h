@@ -51,7 +51,8 @@ extern "C" {
 
 typedef enum {
     AUTOLOCO_OK = 0,
-    AUTOLOCO_E_INVALID = -1, /* null pointer, k or n out of range, unknown dtype or flag */
+    AUTOLOCO_E_INVALID = -1, /* null pointer, k or n out of range, unknown dtype or flag, or a
+                                buffer that is not device memory of the context's device */
     AUTOLOCO_E_ALIGN = -2,   /* a device pointer is not 16-byte aligned */
     AUTOLOCO_E_ALIAS = -3,   /* two device buffers overlap */
     AUTOLOCO_E_DEVICE = -4,  /* the HIP runtime reported an error */
@@ -122,6 +123,10 @@ int autoloco_free(autoloco_ctx* ctx, void* ptr);
 /* ------------------------------------------------------------------------ */
 /* Device buffers of one round                                               */
 /* ------------------------------------------------------------------------ */
+
+/* Every buffer argument of the device calls below must be device (or managed)
+ * memory of the context's device; host memory and memory of another device are
+ * rejected with E_INVALID before anything is launched. */
 
 typedef struct {
     int64_t n;             /* parameters per buffer, n >= 0 */

@@ -71,6 +71,23 @@ int hip_fail(autoloco_ctx* ctx, hipError_t e, const char* what) {
 
 size_t replica_size(int32_t dtype) { return dtype == AUTOLOCO_BF16 ? 2 : 4; }
 
+// The kernels dereference every buffer on the context's device: host memory
+// and memory of another device are rejected before anything is launched.
+int check_device_ptr(autoloco_ctx* ctx, uintptr_t p, const char* name) {
+    hipPointerAttribute_t at;
+    std::memset(&at, 0, sizeof(at));
+    if (hipPointerGetAttributes(&at, reinterpret_cast<const void*>(p)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ctx, AUTOLOCO_E_INVALID, std::string(name) + " is not device memory");
+    }
+    if (at.type == hipMemoryTypeManaged || at.isManaged) return AUTOLOCO_OK;
+    if (at.type != hipMemoryTypeDevice) return fail(ctx, AUTOLOCO_E_INVALID, std::string(name) + " is not device memory");
+    if (at.device != ctx->device)
+        return fail(ctx, AUTOLOCO_E_INVALID, std::string(name) + " is on device " + std::to_string(at.device) +
+                                                 ", the context's is " + std::to_string(ctx->device));
+    return AUTOLOCO_OK;
+}
+
 // Default grid: three workgroups per compute unit, or fewer if fewer fit (the
 // fused kernel's occupancy).  Measured on MI355X (256 CUs) with the round's
 // buffers spread in HBM, 768 workgroups were best or within 1-2 % of best for
@@ -141,6 +158,10 @@ int validate(autoloco_ctx* ctx, const autoloco_buffers* b, bool need_momentum) {
         for (int j = i + 1; j < nr; ++j)
             if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
                 return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    for (int i = 0; i < nr; ++i) {
+        const int st = check_device_ptr(ctx, r[i].lo, r[i].name);
+        if (st != AUTOLOCO_OK) return st;
+    }
     return AUTOLOCO_OK;
 }
 
@@ -250,6 +271,10 @@ int validate_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* b, bool* cop
         for (size_t j = i + 1; j < r.size(); ++j)
             if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
                 return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    for (const Range& x : r) {
+        const int st = check_device_ptr(ctx, x.lo, x.name);
+        if (st != AUTOLOCO_OK) return st;
+    }
     return AUTOLOCO_OK;
 }
 
@@ -282,6 +307,10 @@ int check_ranges(autoloco_ctx* ctx, const std::vector<Range>& r) {
         for (size_t j = i + 1; j < r.size(); ++j)
             if (r[i].lo < r[j].hi && r[j].lo < r[i].hi)
                 return fail(ctx, AUTOLOCO_E_ALIAS, std::string(r[i].name) + " overlaps " + r[j].name);
+    for (const Range& x : r) {
+        const int st = check_device_ptr(ctx, x.lo, x.name);
+        if (st != AUTOLOCO_OK) return st;
+    }
     return AUTOLOCO_OK;
 }
 
@@ -491,6 +520,8 @@ int autoloco_outer_step_bf16(autoloco_ctx* c, const autoloco_buffers* b, const a
         bool alias = hit(b->theta, fbytes) || hit(b->momentum, fbytes);
         for (int k = 0; k < b->k; ++k) alias = alias || hit(b->replicas[k], rbytes);
         if (alias) return fail(c, AUTOLOCO_E_ALIAS, "mean_bf16 overlaps a round buffer");
+        const int ds = check_device_ptr(c, lo, "mean_bf16");
+        if (ds != AUTOLOCO_OK) return ds;
     }
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
@@ -542,6 +573,9 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
         for (int i = 0; i < nr; ++i)
             if ((cp < hi[i] && lo[i] < c_hi) || (sp < hi[i] && lo[i] < s_hi))
                 return fail(c, AUTOLOCO_E_ALIAS, "payload buffers overlap a round buffer");
+        int ds = check_device_ptr(c, cp, "mean_codes");
+        if (ds == AUTOLOCO_OK) ds = check_device_ptr(c, sp, "mean_scales");
+        if (ds != AUTOLOCO_OK) return ds;
     }
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");

@@ -208,6 +208,11 @@ def test_argument_errors(ctx):
     b.k = 17
     assert call(b) == -1
     b.k = 2
+    host = torch.zeros(n, dtype=torch.float32, pin_memory=True)
+    b.grads[1] = host.data_ptr()                                # pinned host memory, not device memory
+    assert call(b) == -1 and "not device memory" in al.autoloco_last_error(ctx)
+    b = al.make_adamw_buffers(dev.params, dev.exp_avg, dev.exp_avg_sq, dev.grads)
+    b.k = 2
     b.n = 0
     assert call(b) == 0 and st.k == 2 and st.clip_coef[0] == 1.0 and st.grad_norm[1] == 0.0
 

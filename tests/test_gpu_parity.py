@@ -289,6 +289,21 @@ def test_rejects_bad_arguments_without_touching_buffers(ctx):
         al.autoloco_round_stats(ctx, dev.theta, [dev.theta], EPS)
 
 
+def test_rejects_host_memory(ctx):
+    # pinned host memory (reachable by the GPU, so a missed check could not fault) in
+    # place of a replica is refused before any launch, with a message
+    n = 4096
+    dev = to_device(cpu_inputs(n, 2, seed=44))
+    host = torch.empty(n, dtype=torch.float32, pin_memory=True)
+    host.fill_(7.0)
+    snap = dev.theta.clone()
+    th, mo = dev.theta.data_ptr(), dev.momentum.data_ptr()
+    assert _raw(ctx, th, mo, [dev.replicas[0].data_ptr(), host.data_ptr()], n, 2) == -1
+    assert "not device memory" in al.autoloco_last_error(ctx)
+    torch.cuda.synchronize()
+    assert torch.equal(dev.theta, snap) and bool((host == 7.0).all())
+
+
 def test_timing_events(ctx):
     inp = to_device(cpu_inputs(1 << 20, 4, seed=43))
     al.autoloco_set_timing(ctx, True)
