@@ -82,7 +82,24 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
+    _build_c_abi_check()
     return LIB
+
+
+C_ABI_SRC = os.path.join(os.path.dirname(PKG), "tests", "c_abi", "round_from_c.c")
+C_ABI_BIN = os.path.join(os.path.dirname(PKG), "tests", "c_abi", "round_from_c")
+
+
+def _build_c_abi_check() -> None:
+    """The plain-C program the tests use to drive a round through the C ABI
+    (gcc, C11, the HIP runtime for device memory; linked against the library)."""
+    if not os.path.exists(C_ABI_SRC):
+        return
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    _run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+          f"-I{rocm}/include", f"-I{INCLUDE}", C_ABI_SRC, "-o", C_ABI_BIN, f"-L{PKG}", "-lautoloco",
+          f"-L{rocm}/lib", "-lamdhip64", "-Wl,-rpath,$ORIGIN/../../paper_2609_36662_amd",
+          f"-Wl,-rpath,{rocm}/lib"])
 
 
 if __name__ == "__main__":
