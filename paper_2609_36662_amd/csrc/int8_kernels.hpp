@@ -58,8 +58,7 @@ __device__ __forceinline__ float codec_q(float x, float s, float r) {
     const float t = x * r;
     float q = __builtin_rintf(t);
     if (!(0.5f - fabsf(t - q) > 6.0e-5f)) q = __builtin_rintf(x / s);
-    q = q < -127.0f ? -127.0f : q;
-    return q > 127.0f ? 127.0f : q;
+    return __builtin_amdgcn_fmed3f(q, -127.0f, 127.0f);   // clip to [-127, 127]
 }
 
 // Maximum over the 64 lanes of a wavefront of a non-negative float (or NaN),
