@@ -125,6 +125,18 @@ def cpu_baseline(sample, coeffs, seconds: float, desc: str, threads: int = 1):
                       f"{done // n}x over {dt:.1f} s (numpy float64, {how})"}
 
 
+def cpu_model() -> str:
+    """Model name of the host CPU (Linux), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def host_threads() -> int:
     """Host cores this process may use, capped at a one-GPU share of 16."""
     try:
@@ -584,6 +596,9 @@ def main() -> int:
         log(f"timing the oracle on the CPU sample: one thread, then {p} threads")
         cpu1 = cpu_baseline(sample, coeffs, args.cpu_seconds, desc)
         cpu = cpu_baseline(sample, coeffs, args.cpu_seconds, desc, threads=p) if p > 1 else cpu1
+        for leg in {id(cpu): cpu, id(cpu1): cpu1}.values():
+            leg["cpu_model"] = cpu_model()
+            leg["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / leg["value"]
 
     out = {
         "metric": METRIC,
