@@ -287,6 +287,9 @@ def bench_inner(args) -> int:
         cpu1 = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc)
         cpu = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc, threads=min(p, k)) \
             if min(p, k) > 1 else cpu1
+        for leg in {id(cpu): cpu, id(cpu1): cpu1}.values():
+            leg["cpu_model"] = cpu_model()
+            leg["gpu_speedup"] = (n * k / (ms_per_step * 1e-3)) / leg["value"]
 
     out = {
         "metric": INNER_METRIC,
