@@ -589,6 +589,23 @@ def main() -> int:
 
     mean_ms = statistics.mean(kernel_ms)
     achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
+
+    # The round's loads and stores without its arithmetic, on the same buffers
+    # with the plain round's launch shape: what the device sustains for this
+    # access pattern (the buffers are left unchanged).
+    reference = None
+    if not args.no_ceiling:
+        ref_ms = []
+        for _ in range(10):
+            al.autoloco_traffic_reference(ctx, inp.theta, inp.momentum, inp.replicas)
+            ref_ms.append(al.autoloco_last_kernel_ms(ctx))
+        ref_bytes = n * (2 * k * s_r + 16)
+        ref_gbs = ref_bytes / (statistics.median(ref_ms) * 1e-3) / 1e9
+        reference = {"kernel": "traffic_kernel (the round's loads and stores, no arithmetic)",
+                     "kernel_ms_median": statistics.median(ref_ms), "bytes": ref_bytes, "gbs": ref_gbs,
+                     "frac_of_peak": ref_gbs / PEAK_HBM_GBS, "round_frac_of_reference": achieved / ref_gbs}
+        log(f"traffic reference (same loads and stores, no arithmetic): {statistics.median(ref_ms):.3f} ms, "
+            f"{ref_gbs:.0f} GB/s; the round runs at {100 * achieved / ref_gbs:.1f} % of it")
     tag = f"round_{rdt}_k{k}_{args.workload}" + ("" if args.codec == "fp32" else f"_{args.codec}")
     traffic = committed_traffic(tag, INT8_SOURCES if args.codec == "int8" else None)
 
@@ -637,6 +654,7 @@ def main() -> int:
         "round_ms_perturbed_median": statistics.median(perturbed_wall) if perturbed_wall else None,
         "perturbed_rounds": len(perturbed_ms),
         "copy_ceiling_gbs": ceiling,
+        "traffic_reference": reference,
         "first_round_stats": {k2: first_stats[k2] for k2 in ("D", "C", "disagreement", "finite")}
         if first_stats else None,
         "cpu_baseline": cpu,

@@ -70,8 +70,8 @@ const char* autoloco_status_string(int status);
 /* ------------------------------------------------------------------------ */
 
 /* A context binds one device and one HIP stream and owns the scratch memory of
- * the two-stage statistics reduction (per-block fp64 partial sums, a block
- * counter and the final sums) plus a pinned host buffer for them.  One context
+ * the two-stage statistics reduction (per-block fp64 partial sums and the
+ * final sums) plus a pinned host buffer for them.  One context
  * serves one stream; calls on one context must not overlap.
  *   device: HIP device ordinal.  stream: a hipStream_t of that device, or NULL
  *   for the default stream.  *out receives the context.
@@ -82,9 +82,11 @@ void autoloco_destroy(autoloco_ctx* ctx);
 /* Message of the last failed call on ctx ("" if none).  Valid until the next call. */
 const char* autoloco_last_error(const autoloco_ctx* ctx);
 
-/* Record HIP events around every round kernel launched through ctx (on the
- * context's stream) so that autoloco_last_kernel_ms() can report the device
- * time of the most recent one.  Off by default. */
+/* Record HIP events around the device work of every call made through ctx (on
+ * the context's stream: the streaming kernel and, when the call returns sums,
+ * the one-workgroup kernel that adds the per-workgroup partials after it) so
+ * that autoloco_last_kernel_ms() can report the device time of the most recent
+ * call.  Off by default. */
 int autoloco_set_timing(autoloco_ctx* ctx, int enable);
 /* Device milliseconds of the last timed launch; waits for it to finish. */
 int autoloco_last_kernel_ms(autoloco_ctx* ctx, float* ms);
@@ -225,6 +227,18 @@ int autoloco_outer_step_bf16(autoloco_ctx* ctx, const autoloco_buffers* bufs,
  * outer interval", start of the local loop).  Asynchronous on the stream.
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
 int autoloco_broadcast_reset(autoloco_ctx* ctx, const autoloco_buffers* bufs);
+
+/* Measurement reference for the fused round (no operation of the paper): the
+ * memory traffic of autoloco_outer_step with FUSE_STATS | FUSE_RESET and none
+ * of its arithmetic.  Same launch shape, same loads and stores in the same
+ * order: theta, the momentum and every replica are read once and each word
+ * is written back unchanged, so all buffers hold their old contents afterwards
+ * (the last n mod 4 parameters are not touched).  Its device time (timing on,
+ * autoloco_last_kernel_ms) is what the device sustains for the round's access
+ * pattern on these buffers: the practical ceiling of the fused round.
+ * Asynchronous on the stream.  Buffers as autoloco_outer_step.
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+int autoloco_traffic_reference(autoloco_ctx* ctx, const autoloco_buffers* bufs);
 
 /* ------------------------------------------------------------------------ */
 /* One GPU's share of a round with one worker replica per GPU                */

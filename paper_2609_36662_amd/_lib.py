@@ -141,6 +141,7 @@ SYMBOLS = [
     ("autoloco_outer_step_bf16", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
+    ("autoloco_traffic_reference", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_rank_payload", C.c_int, [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
                                         C.POINTER(C.c_double)]),
     ("autoloco_shard_step", C.c_int, [C.c_void_p, C.POINTER(ShardBuffers), C.POINTER(OuterCoeffs), C.c_void_p,
@@ -478,6 +479,12 @@ def autoloco_shard_step(ctx: Context, theta, momentum, payloads: Sequence, coeff
 def autoloco_broadcast_reset(ctx: Context, theta, replicas, n=None) -> None:
     b = make_buffers(theta, replicas, None, n)
     _check(lib().autoloco_broadcast_reset(ctx.handle, C.byref(b)), "autoloco_broadcast_reset", ctx)
+
+
+def autoloco_traffic_reference(ctx: Context, theta, momentum, replicas, n=None) -> None:
+    """The fused round's loads and stores without its arithmetic (buffers unchanged)."""
+    b = make_buffers(theta, replicas, momentum, n)
+    _check(lib().autoloco_traffic_reference(ctx.handle, C.byref(b)), "autoloco_traffic_reference", ctx)
 
 
 # -------------------------------------------------------- host scalars --

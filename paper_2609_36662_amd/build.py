@@ -62,6 +62,7 @@ def jobs():
                              f"-DAL_RESET={rs}", "-c", os.path.join(CSRC, "int8_inst.hip"), "-o", obj])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "adamw_inst.hip"), "-o", os.path.join(BUILD, "adamw.o")])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "shard_inst.hip"), "-o", os.path.join(BUILD, "shard.o")])
+    cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "reduce_inst.hip"), "-o", os.path.join(BUILD, "reduce.o")])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "api.hip"), "-o", os.path.join(BUILD, "api.o")])
     for src in ("scalar.cpp", "controller.cpp"):
         cmds.append(["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, src),

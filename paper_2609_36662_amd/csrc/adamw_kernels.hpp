@@ -31,9 +31,7 @@ namespace autoloco {
 struct GradNormArgs {
     const float* grads[kMaxK];
     int64_t n;
-    double* partials;
-    unsigned int* ticket;
-    double* sums;          // [K] squared norms
+    double* partials;      // [gridDim.x][K] per-workgroup squared norms
 };
 
 struct AdamWArgs {
@@ -79,7 +77,7 @@ __global__ void __launch_bounds__(kBlock) grad_norm_kernel(GradNormArgs a) {
             acc[k] += (double)(g * g);
         }
     }
-    grid_reduce<K, kBlock>(acc, a.partials, a.ticket, a.sums);
+    store_partials<K, kBlock>(acc, a.partials);
 }
 
 // Clipping coefficient from a squared norm; NaN stays NaN.

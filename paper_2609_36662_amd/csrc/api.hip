@@ -15,6 +15,7 @@
 #include "shard_kernels.hpp"
 #include "int8_kernels.hpp"
 #include "round_kernels.hpp"
+#include "traffic_kernels.hpp"
 
 using namespace autoloco;
 
@@ -33,7 +34,6 @@ struct autoloco_ctx {
     int occupancy_int8[2][AUTOLOCO_MAX_K + 1] = {};
     int occupancy_bf16p[2][AUTOLOCO_MAX_K + 1] = {};  // the BF16-payload round
     double* partials = nullptr;
-    unsigned int* ticket = nullptr;
     double* sums = nullptr;
     double* host_sums = nullptr;
     bool timing = false;
@@ -209,8 +209,6 @@ RoundArgs make_args(autoloco_ctx* ctx, const autoloco_buffers* b) {
     a.scale = 1.f;
     a.inv_k = 1.0f / static_cast<float>(b->k);
     a.partials = ctx->partials;
-    a.ticket = ctx->ticket;
-    a.sums = ctx->sums;
     return a;
 }
 
@@ -224,6 +222,9 @@ int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, 
         return hip_fail(ctx, e, "hipEventRecord");
     e = launcher(b->replica_dtype, mode)(b->k, blocks, ctx->stream, a);
     if (e != hipSuccess) return hip_fail(ctx, e, "kernel launch");
+    if (stats && (e = launch_finish_sums(2 * b->k + 1, kBlock, blocks, ctx->partials, ctx->sums, ctx->stream)) !=
+                     hipSuccess)
+        return hip_fail(ctx, e, "reduction launch");
     if (ctx->timing) {
         if ((e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
         ctx->timed_valid = true;
@@ -314,13 +315,16 @@ int check_ranges(autoloco_ctx* ctx, const std::vector<Range>& r) {
     return AUTOLOCO_OK;
 }
 
-// Launches a kernel that leaves one float64 sum in ctx->sums; with out, waits
-// for it and stores it.
+// Launches a kernel of `blocks` workgroups that leaves one float64 partial sum
+// per workgroup, then the reduction of those into ctx->sums[0]; with out,
+// waits for it and stores it.
 template <typename Launch>
-int run_one_sum(autoloco_ctx* c, Launch launch, double* out) {
+int run_one_sum(autoloco_ctx* c, Launch launch, int blocks, double* out) {
     hipError_t e;
     if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     if ((e = launch()) != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if ((e = launch_finish_sums(1, kBlock, blocks, c->partials, c->sums, c->stream)) != hipSuccess)
+        return hip_fail(c, e, "reduction launch");
     if (c->timing) {
         if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
         c->timed_valid = true;
@@ -381,10 +385,9 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
         c->occupancy_bf16p[1][k] = occupancy_round_bf16_m8(k);
     }
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
-              hipMalloc(&c->ticket, 256) == hipSuccess &&
               hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
               hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocDefault) == hipSuccess;
-    ok = ok && hipMemset(c->ticket, 0, 256) == hipSuccess && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
+    ok = ok && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
     ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess &&
          hipEventCreate(&c->ev_mid) == hipSuccess;
     ok = ok && hipDeviceSynchronize() == hipSuccess;
@@ -402,7 +405,6 @@ void autoloco_destroy(autoloco_ctx* c) {
         DeviceGuard g(c->device);
         (void)hipStreamSynchronize(c->stream);
         if (c->partials) (void)hipFree(c->partials);
-        if (c->ticket) (void)hipFree(c->ticket);
         if (c->sums) (void)hipFree(c->sums);
         if (c->host_sums) (void)hipHostFree(c->host_sums);
         if (c->ev_start) (void)hipEventDestroy(c->ev_start);
@@ -592,8 +594,6 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
     a.mean_codes = codes;
     a.mean_scales = scales;
     a.partials = c->partials;
-    a.ticket = c->ticket;
-    a.sums = c->sums;
     const int rt = b->replica_dtype == AUTOLOCO_BF16 ? 1 : 0;
     int per_cu = c->occupancy_int8[rt][b->k];
     if (per_cu < 1) per_cu = 1;
@@ -607,6 +607,9 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
     if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     e = table[rt][stats ? 1 : 0][reset ? 1 : 0](b->k, blocks, c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if (stats && (e = launch_finish_sums(2 * b->k + 1, kInt8Threads, blocks, c->partials, c->sums, c->stream)) !=
+                     hipSuccess)
+        return hip_fail(c, e, "reduction launch");
     if (c->timing) {
         if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
         c->timed_valid = true;
@@ -635,6 +638,27 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
     hipError_t e;
     if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if (c->timing) {
+        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+        c->timed_valid = true;
+        c->adamw_timed = false;
+    }
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+int autoloco_traffic_reference(autoloco_ctx* c, const autoloco_buffers* b) {
+    int st = validate(c, b, true);
+    if (st != AUTOLOCO_OK) return st;
+    if (b->n == 0) return AUTOLOCO_OK;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    RoundArgs a = make_args(c, b);
+    const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k);
+    hipError_t e;
+    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    e = launch_traffic(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a, 0u);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
     if (c->timing) {
         if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
@@ -732,11 +756,9 @@ int autoloco_rank_payload(autoloco_ctx* c, int64_t n, const float* theta, const 
     a.payload = payload;
     a.n = n;
     a.partials = c->partials;
-    a.ticket = c->ticket;
-    a.sums = c->sums;
     const int blocks = blocks8(c, n);
     const int rt = dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32;
-    return run_one_sum(c, [&] { return launch_rank_payload(rt, blocks, c->stream, a); }, sq_norm);
+    return run_one_sum(c, [&] { return launch_rank_payload(rt, blocks, c->stream, a); }, blocks, sq_norm);
 }
 
 int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const autoloco_outer_coeffs* co,
@@ -777,11 +799,9 @@ int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const 
     a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
     a.inv_k64 = 1.0 / static_cast<double>(b->k);
     a.partials = c->partials;
-    a.ticket = c->ticket;
-    a.sums = c->sums;
     const int blocks = blocks8(c, b->n);
     const int k = b->k;
-    return run_one_sum(c, [&] { return launch_shard_step(k, blocks, c->stream, a); }, sq_mean);
+    return run_one_sum(c, [&] { return launch_shard_step(k, blocks, c->stream, a); }, blocks, sq_mean);
 }
 
 int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const autoloco_adamw_coeffs* co,
@@ -816,10 +836,11 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
         for (int k = 0; k < b->k; ++k) na.grads[k] = b->grads[k];
         na.n = b->n;
         na.partials = c->partials;
-        na.ticket = c->ticket;
-        na.sums = c->sums;
-        e = launch_grad_norm(b->k, blocks_for(c, b->n, AUTOLOCO_F32, b->k), c->stream, na);
+        const int nblocks = blocks_for(c, b->n, AUTOLOCO_F32, b->k);
+        e = launch_grad_norm(b->k, nblocks, c->stream, na);
         if (e != hipSuccess) return hip_fail(c, e, "gradient norm launch");
+        e = launch_finish_sums(b->k, kBlock, nblocks, c->partials, c->sums, c->stream);
+        if (e != hipSuccess) return hip_fail(c, e, "reduction launch");
     }
     if (c->timing && (e = hipEventRecord(c->ev_mid, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     AdamWArgs a;
@@ -909,6 +930,42 @@ hipError_t launch_reset(int rt, int k, int blocks, hipStream_t s, const RoundArg
         case 14: return reset_k<14>(rt, blocks, s, a);
         case 15: return reset_k<15>(rt, blocks, s, a);
         case 16: return reset_k<16>(rt, blocks, s, a);
+        default: return hipErrorInvalidValue;
+    }
+}
+}  // namespace autoloco
+
+// -------------------------------------------------------- traffic launcher
+namespace autoloco {
+namespace {
+template <int K>
+hipError_t traffic_k(int rt, int blocks, hipStream_t s, const RoundArgs& a, uint32_t mask) {
+    if (rt == RT_BF16)
+        hipLaunchKernelGGL((traffic_kernel<K, RT_BF16>), dim3(blocks), dim3(kBlock), 0, s, a, mask);
+    else
+        hipLaunchKernelGGL((traffic_kernel<K, RT_F32>), dim3(blocks), dim3(kBlock), 0, s, a, mask);
+    return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_traffic(int rt, int k, int blocks, hipStream_t s, const RoundArgs& a, uint32_t mask) {
+    switch (k) {
+        case 1: return traffic_k<1>(rt, blocks, s, a, mask);
+        case 2: return traffic_k<2>(rt, blocks, s, a, mask);
+        case 3: return traffic_k<3>(rt, blocks, s, a, mask);
+        case 4: return traffic_k<4>(rt, blocks, s, a, mask);
+        case 5: return traffic_k<5>(rt, blocks, s, a, mask);
+        case 6: return traffic_k<6>(rt, blocks, s, a, mask);
+        case 7: return traffic_k<7>(rt, blocks, s, a, mask);
+        case 8: return traffic_k<8>(rt, blocks, s, a, mask);
+        case 9: return traffic_k<9>(rt, blocks, s, a, mask);
+        case 10: return traffic_k<10>(rt, blocks, s, a, mask);
+        case 11: return traffic_k<11>(rt, blocks, s, a, mask);
+        case 12: return traffic_k<12>(rt, blocks, s, a, mask);
+        case 13: return traffic_k<13>(rt, blocks, s, a, mask);
+        case 14: return traffic_k<14>(rt, blocks, s, a, mask);
+        case 15: return traffic_k<15>(rt, blocks, s, a, mask);
+        case 16: return traffic_k<16>(rt, blocks, s, a, mask);
         default: return hipErrorInvalidValue;
     }
 }

@@ -38,9 +38,7 @@ struct Int8Args {
     double inv_k;
     int8_t* mean_codes;   // [n] or null
     float* mean_scales;   // [ceil(n / 4096)] or null
-    double* partials;
-    unsigned int* ticket;
-    double* sums;
+    double* partials;     // [gridDim.x][2K+1] per-workgroup sums
 };
 
 __device__ __forceinline__ float codec_scale(float amax) {
@@ -420,7 +418,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     // the shorter last block belongs to the workgroup the grid stride gives it
     if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{});
 
-    if constexpr (STATS) grid_reduce<NS, NT>(acc, a.partials, a.ticket, a.sums);
+    if constexpr (STATS) store_partials<NS, NT>(acc, a.partials);
 }
 
 typedef hipError_t (*Int8Launcher)(int k, int blocks, hipStream_t stream, const Int8Args& a);

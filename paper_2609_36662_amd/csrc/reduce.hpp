@@ -1,8 +1,8 @@
 // Deterministic reductions of per-thread fp64 sums, shared by the streaming
 // kernels.  Every stage adds in a fixed order (wavefront butterfly, the waves
-// of a workgroup in index order through LDS, the workgroups in index order in
-// the last workgroup to finish), so with a fixed grid the result is the same
-// bit for bit on every run.
+// of a workgroup in index order through LDS, then the workgroups' partials in
+// index order in a one-workgroup finishing kernel), so with a fixed grid the
+// result is the same bit for bit on every run.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -42,38 +42,36 @@ __device__ __forceinline__ double block_reduce(double (&acc)[NS], double* lds) {
     return t;
 }
 
-// Stage 1 writes this workgroup's partial sums; the last workgroup to arrive
-// (agent-scope ticket) adds all partials in workgroup order into sums[] and
-// resets the ticket for the next launch.
+// Stage 1: this workgroup's sums into partials[blockIdx.x][NS] with plain
+// stores.  Stage 2 is finish_sums_kernel, launched after the producing kernel
+// on the same stream (the stream order makes the partials visible to it), so
+// no workgroup takes a device-scope fence or a ticket at its end.
 template <int NS, int NT>
-__device__ __forceinline__ void grid_reduce(double (&acc)[NS], double* partials, unsigned int* ticket,
-                                            double* sums) {
+__device__ __forceinline__ void store_partials(double (&acc)[NS], double* partials) {
     __shared__ double lds[kMaxWaves * kMaxSums];
-    __shared__ int is_last;
     const double part = block_reduce<NS, NT>(acc, lds);
-    if (threadIdx.x < NS)
-        __hip_atomic_store(&partials[(int64_t)blockIdx.x * NS + threadIdx.x], part, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned int prev = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        is_last = (prev == gridDim.x - 1);
-    }
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();
+    if (threadIdx.x < NS) partials[(int64_t)blockIdx.x * NS + threadIdx.x] = part;
+}
+
+// Stage 2, one workgroup of NT threads (NT = the producer's workgroup size):
+// thread t adds the partials of workgroups t, t + NT, ... in that order, then
+// the workgroup reduces those as in stage 1; sums[0..NS) receives the totals.
+template <int NS, int NT>
+__global__ void __launch_bounds__(NT) finish_sums_kernel(const double* partials, int nblocks, double* sums) {
+    __shared__ double lds[kMaxWaves * kMaxSums];
     double tot[NS];
 #pragma unroll
     for (int j = 0; j < NS; ++j) tot[j] = 0.0;
-    for (unsigned int b = threadIdx.x; b < gridDim.x; b += NT) {
+    for (int b = threadIdx.x; b < nblocks; b += NT) {
 #pragma unroll
-        for (int j = 0; j < NS; ++j)
-            tot[j] += __hip_atomic_load(&partials[(int64_t)b * NS + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int j = 0; j < NS; ++j) tot[j] += partials[(int64_t)b * NS + j];
     }
     const double fin = block_reduce<NS, NT>(tot, lds);
     if (threadIdx.x < NS) sums[threadIdx.x] = fin;
-    if (threadIdx.x == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+
+// Launches finish_sums_kernel for ns in 1..kMaxSums and nt in {256, 512}.
+hipError_t launch_finish_sums(int ns, int nt, int nblocks, const double* partials, double* sums,
+                              hipStream_t stream);
 
 }  // namespace autoloco

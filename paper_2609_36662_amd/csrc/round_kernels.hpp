@@ -18,10 +18,11 @@
 // grid.  Elementwise arithmetic is fp32; the squared sums of one vector are
 // added in fp32 and then into per-lane fp64 running sums.  The 2K+1 sums are
 // reduced deterministically: a wavefront butterfly, then the waves of the
-// workgroup in order through LDS into one partial per workgroup, then the
-// last workgroup to finish (found with an atomic counter) adds the partials
-// in workgroup order.  With the grid fixed, every run adds the same numbers
-// in the same order, so the statistics are bit-identical between runs.
+// workgroup in order through LDS into one partial per workgroup (a plain
+// store), then a one-workgroup kernel launched after this one on the same
+// stream adds the partials in workgroup order.  With the grid fixed, every
+// run adds the same numbers in the same order, so the statistics are
+// bit-identical between runs.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -50,9 +51,7 @@ struct RoundArgs {
     void* replicas[kMaxK];
     int64_t n;
     float mu, eta, scale, inv_k;
-    double* partials;      // [gridDim.x][2K+1]
-    unsigned int* ticket;  // zero between launches
-    double* sums;          // [2K+1] final sums
+    double* partials;      // [gridDim.x][2K+1] per-workgroup sums
     uint16_t* payload;     // BF16 payload modes: [n] bits of the received mean, or null
     double inv_k64;        // 1/K in float64 (BF16 payload modes)
 };
@@ -318,7 +317,7 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
         }
     }
 
-    if constexpr (STATS) grid_reduce<NS, kBlock>(acc, a.partials, a.ticket, a.sums);
+    if constexpr (STATS) store_partials<NS, kBlock>(acc, a.partials);
 }
 
 // ------------------------------------------------------------ reset kernel --

@@ -28,9 +28,7 @@ struct RankPayloadArgs {
     const void* replica;
     uint16_t* payload;
     int64_t n;
-    double* partials;
-    unsigned int* ticket;
-    double* sums;
+    double* partials;     // [gridDim.x] per-workgroup sums
 };
 
 struct ShardArgs {
@@ -41,9 +39,7 @@ struct ShardArgs {
     int64_t n;
     float mu, eta, scale;
     double inv_k64;
-    double* partials;
-    unsigned int* ticket;
-    double* sums;
+    double* partials;     // [gridDim.x] per-workgroup sums
 };
 
 // Both kernels walk runs of 4 parameters ("quads"); a lane owns two quads per
@@ -98,7 +94,7 @@ __global__ void __launch_bounds__(kBlock) rank_payload_kernel(RankPayloadArgs a)
         acc[0] += (double)(d * d);
         a.payload[j] = (uint16_t)bf16_rne(d);
     }
-    grid_reduce<1, kBlock>(acc, a.partials, a.ticket, a.sums);
+    store_partials<1, kBlock>(acc, a.partials);
 }
 
 // The received mean of one parameter from its K payloads, and the step.
@@ -170,7 +166,7 @@ __global__ void __launch_bounds__(kBlock) shard_step_kernel(ShardArgs a) {
         a.momentum[j] = v_new;
         if (a.mean_out != nullptr) a.mean_out[j] = (uint16_t)pb;
     }
-    grid_reduce<1, kBlock>(acc, a.partials, a.ticket, a.sums);
+    store_partials<1, kBlock>(acc, a.partials);
 }
 
 hipError_t launch_rank_payload(int rt, int blocks, hipStream_t s, const RankPayloadArgs& a);
