@@ -47,16 +47,33 @@ __device__ __forceinline__ float codec_scale(float amax) {
     return s < 0x1p-126f ? 0x1p-126f : s;
 }
 
-// Code of x at scale s (r = fp32(1/s)): the integer nearest fp32(x / s), ties
-// to even, clipped to +-127.  t = x * r differs from fp32(x / s) by at most
-// 1.5 * 2^-23 * |x / s| <= 2.3e-5 here (|x / s| <= 127), so rint(t) is the
-// same integer unless t lies within that distance of a half-integer; only
-// then (about 1e-4 of the elements) is the IEEE quotient formed.
-__device__ __forceinline__ float codec_q(float x, float s, float r) {
-    const float t = x * r;
-    float q = __builtin_rintf(t);
-    if (!(0.5f - fabsf(t - q) > 6.0e-5f)) q = __builtin_rintf(x / s);
-    return __builtin_amdgcn_fmed3f(q, -127.0f, 127.0f);   // clip to [-127, 127]
+// Codes of x[0..NV) at scale s (r = fp32(1/s)): the integers nearest
+// fp32(x / s), ties to even, clipped to +-127.  t = x * r differs from
+// fp32(x / s) by at most 1.5 * 2^-23 * |x / s| <= 2.3e-5 here (|x / s| <= 127),
+// so rint(t) is the same integer unless t lies within that distance of a
+// half-integer; only then (about 1e-4 of the elements) is the IEEE quotient
+// formed.  The test runs for every element first and the quotients are taken
+// behind one wavefront-uniform branch, entered only when some lane of the
+// wavefront needs one, so the common path has no per-element branch.
+// x(e) gives element e (evaluated again on the rare path).
+template <int NV, typename X>
+__device__ __forceinline__ void codec_q(X x, float s, float r, float (&q)[NV]) {
+    bool bad[NV];
+    bool any = false;
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        const float t = x(e) * r;
+        q[e] = __builtin_rintf(t);
+        bad[e] = !(0.5f - fabsf(t - q[e]) > 6.0e-5f);
+        any = any || bad[e];
+    }
+    if (__builtin_amdgcn_ballot_w64(any) != 0) {
+#pragma unroll
+        for (int e = 0; e < NV; ++e)
+            if (bad[e]) q[e] = __builtin_rintf(x(e) / s);
+    }
+#pragma unroll
+    for (int e = 0; e < NV; ++e) q[e] = __builtin_amdgcn_fmed3f(q[e], -127.0f, 127.0f);   // clip to [-127, 127]
 }
 
 // Maximum over the 64 lanes of a wavefront of a non-negative float (or NaN),
@@ -284,8 +301,10 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         for (int k = 0; k < K; ++k) {
             const float s = codec_scale(amax[k]);
             const float r = 1.0f / s;
+            float q[V];
+            codec_q<V>([&](int e) { return D(k, e); }, s, r, q);
 #pragma unroll
-            for (int e = 0; e < V; ++e) sum[e] += (double)(codec_q(D(k, e), s, r) * s);
+            for (int e = 0; e < V; ++e) sum[e] += (double)(q[e] * s);
         }
         float mean[V];
         float mmax[1] = {0.f};
@@ -299,11 +318,9 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         const float rm = 1.0f / sm;
 
         float agg[V], qm[V];
+        codec_q<V>([&](int e) { return mean[e]; }, sm, rm, qm);
 #pragma unroll
-        for (int e = 0; e < V; ++e) {
-            qm[e] = codec_q(mean[e], sm, rm);
-            agg[e] = ok[e] ? qm[e] * sm : 0.0f;
-        }
+        for (int e = 0; e < V; ++e) agg[e] = ok[e] ? qm[e] * sm : 0.0f;
         if (a.mean_codes != nullptr) {
 #pragma unroll
             for (int g = 0; g < G; ++g) {
