@@ -444,6 +444,128 @@ def bench_share(args) -> int:
     return 0
 
 
+CLOSED_LOOP_METRIC = ("closed-loop sync-round params/s (round + interval controller) and achieved HBM GB/s "
+                      "(% of peak), 7B params K=4, 20 rounds")
+
+
+def bench_closed_loop(args) -> int:
+    """Consecutive rounds with the interval controller in the loop: each round's
+    fused outer step runs with the coefficients of the controller's decision,
+    and its statistics are the controller's next observation.  Between rounds
+    (untimed), every worker endpoint is drawn around the new synchronised
+    parameters, the drift growing with the learning-rate mass of the selected
+    interval, with a per-round jitter of the per-worker part and, in the first
+    assessed interval from round 12 on, a fault (per-worker part x10) that the
+    controller must answer with a shorter horizon.  A timed step runs from the
+    synchronisation before the round to the decision for the next interval."""
+    import math
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift, shapes
+
+    shape_name, k, rdt = WORKLOADS[args.workload][0], WORKLOADS[args.workload][1], WORKLOADS[args.workload][2]
+    if args.k:
+        k = args.k
+    n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
+    s_r = 4 if rdt == "f32" else 2
+    bytes_per_round = n * (2 * k * s_r + 16)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"closed loop {args.workload}: n={n:,} K={k} replicas={rdt}, {args.warmup} + {args.steps} rounds, "
+        f"bytes/round={bytes_per_round / 1e9:.3f} GB")
+    ctx = al.autoloco_create(0)
+    ts, spread = al.spread_tensors(ctx, n, [torch.float32, torch.float32] + [tdtype] * k)
+    inp = drift.RoundInputs(ts[0], ts[1], ts[2:])
+    drift.fill_theta_momentum(inp, seed=42)
+    if args.grid:
+        al.autoloco_set_grid_limit(ctx, args.grid)
+    al.autoloco_set_timing(ctx, True)
+    ctl = al.autoloco_controller_create()
+    dec = al.autoloco_select_interval(ctl, None)
+    lam1 = dec.lambda_sel
+    tokens_per_step = float(1 << 20)
+    assessed = (4, 5, 6)   # autoloco_phase: monitoring and the two candidate phases
+    fault_done = False
+    walls, kms, trace = [], [], []
+    sample = None
+    for r in range(args.warmup + args.steps):
+        lam = dec.lambda_sel
+        fault = not fault_done and r >= 12 and dec.phase in assessed
+        jit = math.exp(0.05 * math.sin(1.7 * r + 0.3)) * (10.0 if fault else 1.0)
+        drift.fill_replicas(inp, seed=100 + r, scale=lam / lam1, indep_scale=[jit] * k)
+        if r == args.warmup and not args.no_cpu_baseline:
+            import numpy as np
+            m = min(n, args.cpu_sample)
+
+            def host(tn):
+                x = tn[:m].cpu()
+                return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
+            sample = ((host(inp.theta), host(inp.momentum), [host(x) for x in inp.replicas], rdt), dec.coeffs)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st = al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, dec.coeffs,
+                                    al.FUSE_STATS | al.FUSE_RESET, 1e-12)
+        prev = dec
+        dec = al.autoloco_select_interval(ctl, al.make_observation(st.D, st.C, lam, tokens_per_step * prev.h_step,
+                                                                   prev.h_step, st.finite))
+        wall = (time.perf_counter() - t0) * 1e3
+        if fault:
+            fault_done = True
+        if r >= args.warmup:
+            walls.append(wall)
+            kms.append(al.autoloco_last_kernel_ms(ctx))
+        trace.append({"round": r, "h_step": prev.h_step, "rho": prev.coeffs.rho, "D": st.D, "C": st.C,
+                      "assessment_after": dec.assessment, "next_h_step": dec.h_step, "fault": fault})
+        log(f"round {r}: H^step {prev.h_step} rho {prev.coeffs.rho:.4f} D {st.D:.4g} C {st.C:.4g} -> "
+            f"assessment {dec.assessment}, next H^step {dec.h_step}; {wall:.3f} ms" + (" (fault)" if fault else ""))
+    ms_per_step = statistics.mean(walls)
+    mean_ms = statistics.mean(kms)
+    achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
+    cpu = None
+    if sample is not None:
+        log(f"timing the oracle on the CPU sample ({host_threads()} threads)")
+        cpu = cpu_baseline(sample[0], sample[1], args.cpu_seconds, f"{args.workload} K={k} {rdt} closed loop",
+                           threads=host_threads())
+        cpu["cpu_model"] = cpu_model()
+        cpu["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / cpu["value"]
+    tag = f"round_{rdt}_k{k}_{args.workload}"
+    out = {
+        "metric": CLOSED_LOOP_METRIC,
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if rdt == "f32" else "f32 (bf16 replicas)",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload} closed loop: {n:,} parameters, K={k} {rdt} replicas, fused stats + "
+                        f"Nesterov + reset with the coefficients the interval controller chose, the controller "
+                        f"fed each round's statistics (C4 settings, budget 50,000 steps)",
+            "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
+            "alloc": "spread" if spread else "plain", "fault_round": next((t["round"] for t in trace if t["fault"]), None),
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": committed_traffic(tag),
+        },
+        "kernel_ms_mean": mean_ms,
+        "round_ms_max": max(walls),
+        "rounds": trace,
+        "cpu_baseline": cpu,
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+    del inp, ts
+    ctx.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -465,9 +587,11 @@ def main() -> int:
     ap.add_argument("--no-ceiling", action="store_true")
     ap.add_argument("--perturbed", type=int, default=20,
                     help="extra rounds, each on freshly drawn replicas (drawn outside the timing)")
-    ap.add_argument("--step", choices=("round", "inner", "share"), default="round",
+    ap.add_argument("--step", choices=("round", "inner", "share", "closed-loop"), default="round",
                     help="round: the synchronisation round; inner: one AdamW step of every worker; share: one "
-                         "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives)")
+                         "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives); "
+                         "closed-loop: consecutive rounds with the interval controller choosing each one's "
+                         "coefficients from the previous round's statistics (use --workload llama-7b)")
     ap.add_argument("--copy", action="store_true", help="inner: also write each worker's BF16 compute copy")
     args = ap.parse_args()
 
@@ -480,6 +604,8 @@ def main() -> int:
         return bench_inner(args)
     if args.step == "share":
         return bench_share(args)
+    if args.step == "closed-loop":
+        return bench_closed_loop(args)
 
     import torch
     import paper_2609_36662_amd as al

@@ -173,6 +173,26 @@ def test_grid_size_changes_only_rounding(ctx):
         al.autoloco_set_grid_limit(ctx, 0)
 
 
+def test_largest_grid(ctx):
+    # 16,384 workgroups (the scratch capacity): every partial slot in use, and the
+    # finishing kernel's strided loop runs 64 times per thread
+    n, k = 17_000_003, 4
+    inp = cpu_inputs(n, k, seed=19)
+    dev = to_device(inp)
+    c = _tiny_coeffs(True)
+    ref = _oracle_round(inp, c)
+    try:
+        al.autoloco_set_grid_limit(ctx, 16384)
+        assert al.autoloco_launch_shape(ctx, n, k)[0] == 16384
+        st = al.autoloco_outer_step(ctx, dev.theta, dev.momentum, dev.replicas, c, al.FUSE_STATS | al.FUSE_RESET, EPS)
+        torch.cuda.synchronize()
+    finally:
+        al.autoloco_set_grid_limit(ctx, 0)
+    assert_stats_close(st, ref.stats)
+    assert_close_elementwise(dev.theta.cpu().numpy(), ref.theta, what="theta'")
+    assert_close_elementwise(dev.momentum.cpu().numpy(), ref.momentum, what="v'")
+
+
 def test_broadcast_reset(ctx):
     for dtype in (torch.float32, torch.bfloat16):
         n, k = 777_777, 5
