@@ -64,7 +64,7 @@ __device__ __forceinline__ void codec_q(X x, float s, float r, float (&q)[NV]) {
     for (int e = 0; e < NV; ++e) {
         const float t = x(e) * r;
         q[e] = __builtin_rintf(t);
-        bad[e] = !(0.5f - fabsf(t - q[e]) > 6.0e-5f);
+        bad[e] = !(fabsf(t - q[e]) < 0.5f - 6.0e-5f);   // also true for NaN
         any = any || bad[e];
     }
     if (__builtin_amdgcn_ballot_w64(any) != 0) {
