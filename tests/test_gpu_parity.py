@@ -159,6 +159,43 @@ def test_statistics_bit_stable_across_runs(ctx):
     assert all(o == outs[0] for o in outs[1:])
 
 
+_CHILD = """
+import sys
+sys.path.insert(0, {root!r})
+import hashlib, torch
+import paper_2609_36662_amd as al
+from tests.gpu_common import cpu_inputs, to_device
+dev = to_device(cpu_inputs({n}, {k}, seed=23))
+ctx = al.autoloco_create(0)
+st = al.autoloco_round_stats(ctx, dev.theta, dev.replicas, 1e-12)
+c = al.autoloco_outer_correction(al.make_outer_cfg(normalize=True), 2.0e-2, 1.25e-2)
+st2 = al.autoloco_outer_step(ctx, dev.theta, dev.momentum, dev.replicas, c, al.FUSE_STATS | al.FUSE_RESET, 1e-12)
+h = hashlib.sha256(dev.theta.cpu().numpy().tobytes() + dev.momentum.cpu().numpy().tobytes()).hexdigest()
+print(bytes(st).hex(), bytes(st2).hex(), h)
+ctx.close()
+"""
+
+
+def test_statistics_bit_stable_across_processes(ctx):
+    # the same round in a fresh process gives the same bits (statistics, theta', v')
+    import hashlib
+    import os
+    import subprocess
+    import sys
+    n, k = 2_500_001, 8
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    dev = to_device(cpu_inputs(n, k, seed=23))
+    st = al.autoloco_round_stats(ctx, dev.theta, dev.replicas, EPS)
+    c = al.autoloco_outer_correction(al.make_outer_cfg(normalize=True), 2.0e-2, 1.25e-2)
+    st2 = al.autoloco_outer_step(ctx, dev.theta, dev.momentum, dev.replicas, c, al.FUSE_STATS | al.FUSE_RESET, EPS)
+    h = hashlib.sha256(dev.theta.cpu().numpy().tobytes() + dev.momentum.cpu().numpy().tobytes()).hexdigest()
+    print(f"child process: n={n} k={k}", flush=True)
+    p = subprocess.run([sys.executable, "-c", _CHILD.format(root=root, n=n, k=k)], capture_output=True, text=True,
+                       timeout=100)
+    assert p.returncode == 0, p.stderr[-2000:]
+    assert p.stdout.split() == [bytes(st).hex(), bytes(st2).hex(), h]
+
+
 def test_grid_size_changes_only_rounding(ctx):
     n, k = 2_000_003, 4
     inp = cpu_inputs(n, k, seed=17)
