@@ -3,9 +3,9 @@
 The codes and block scales of the encoded mean are integers and FP32 values
 decided by FP32 arithmetic the paper fixes, so they must match the oracle bit
 for bit; θ', v' and the statistics match within the round's tolerances.  At
-the full 1.1B size the codec is checked block by block on sampled codec
-blocks (the codec is local to a block), and D against the plain statistics
-pass."""
+the full 1.1B (fp32 replicas) and 3B (bf16 replicas) sizes the codec is
+checked block by block on sampled codec blocks (the codec is local to a
+block), and D against the plain statistics pass."""
 import numpy as np
 import pytest
 import torch
@@ -129,24 +129,25 @@ def test_payload_argument_checks(ctx):
              None) == -1                                                  # only one payload buffer
 
 
-def test_llama_1b1_sampled_codec_blocks(ctx):
-    n, k = shapes.llama_1b1().n_params, 8
-    ts, _ = al.spread_tensors(ctx, n, [torch.float32] * (k + 2))
+def _sampled_codec_blocks(ctx, shape, k, dtype, normalize, seed):
+    n = shapes.SHAPES[shape]().n_params
+    ts, _ = al.spread_tensors(ctx, n, [torch.float32] * 2 + [dtype] * k)
     inp = drift.RoundInputs(ts[0], ts[1], ts[2:])
     drift.fill_theta_momentum(inp, seed=42)
     drift.fill_replicas(inp, seed=42)
     nb = (n + 4095) // 4096
-    rng = np.random.default_rng(3)
+    rng = np.random.default_rng(seed)
     blocks = sorted(set(rng.integers(0, nb, 48).tolist()) | {0, nb - 1})
     saved = {}
     for b in blocks:
         lo, hi = b * 4096, min(n, (b + 1) * 4096)
         saved[b] = (inp.theta[lo:hi].cpu().numpy(), inp.momentum[lo:hi].cpu().numpy(),
-                    [r[lo:hi].cpu().numpy() for r in inp.replicas])
+                    [host_array(r[lo:hi]) for r in inp.replicas])
     plain = al.autoloco_round_stats(ctx, inp.theta, inp.replicas, EPS)
     codes = torch.empty(n, dtype=torch.int8, device="cuda")
     scales = torch.empty(nb, dtype=torch.float32, device="cuda")
-    c = al.make_coeffs(COEFFS["mu"], COEFFS["eta_out"], COEFFS["rho"], False)
+    c = al.make_coeffs(COEFFS["mu"], COEFFS["eta_out"], COEFFS["rho"], normalize)
+    print(f"{shape}: n={n:,} K={k} {dtype}, {len(blocks)} sampled codec blocks", flush=True)
     st = al.autoloco_outer_step_int8(ctx, inp.theta, inp.momentum, inp.replicas, c, al.FUSE_STATS | al.FUSE_RESET,
                                      EPS, mean_codes=codes, mean_scales=scales)
     torch.cuda.synchronize()
@@ -157,10 +158,24 @@ def test_llama_1b1_sampled_codec_blocks(ctx):
     for b in blocks:
         lo, hi = b * 4096, min(n, (b + 1) * 4096)
         th, mo, reps = saved[b]
-        ref = ic.int8_round(th, mo, reps, c.mu, c.eta_out, c.rho, False, EPS)
+        ref = ic.int8_round(th, mo, reps, c.mu, c.eta_out, c.rho, normalize, EPS)
         assert np.array_equal(codes[lo:hi].cpu().numpy(), ref.mean_codes), b
         assert scales[b].cpu().numpy().view(np.uint32) == ref.mean_scales.view(np.uint32)[0], b
-        assert_close_elementwise(inp.theta[lo:hi].cpu().numpy(), ref.theta, what=f"theta' block {b}")
+        got_th = inp.theta[lo:hi].cpu().numpy()
+        assert_close_elementwise(got_th, ref.theta, what=f"theta' block {b}")
         assert_close_elementwise(inp.momentum[lo:hi].cpu().numpy(), ref.momentum, what=f"v' block {b}")
+        for r in inp.replicas:
+            if dtype == torch.float32:
+                assert np.array_equal(r[lo:hi].cpu().numpy().view(np.uint32), got_th.view(np.uint32)), b
+            else:
+                assert np.array_equal(bits16(r[lo:hi]), bits16(inp.theta[lo:hi].to(torch.bfloat16))), b
     del inp, ts
     torch.cuda.empty_cache()
+
+
+def test_llama_1b1_sampled_codec_blocks(ctx):
+    _sampled_codec_blocks(ctx, "llama-1.1b", 8, torch.float32, False, seed=3)
+
+
+def test_llama_3b_bf16_sampled_codec_blocks(ctx):
+    _sampled_codec_blocks(ctx, "llama-3b", 8, torch.bfloat16, True, seed=5)
