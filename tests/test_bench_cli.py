@@ -19,5 +19,5 @@ def test_help_lists_the_modes():
     p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"], capture_output=True, text=True,
                        timeout=120)
     assert p.returncode == 0
-    for word in ("--codec", "--step", "--workload", "--steps", "--warmup"):
+    for word in ("--codec", "--step", "--workload", "--steps", "--warmup", "closed-loop", "inner", "share"):
         assert word in p.stdout
