@@ -130,10 +130,15 @@ struct BoolC {
 // (1 KB of fp32, 512 B of bf16) and no cache line is written in parts.  The loop runs over the full blocks, in which
 // every load and store is a whole vector; the one shorter last block, if any,
 // goes through a second instance of the same body with per-element accesses.
-// Up to 8 bf16 workers, the raw replica words and theta of a workgroup's next
-// block are loaded while the current one is encoded (the block barriers wait
-// for LDS traffic only), and pseudo-gradients are formed from the raw words
-// where they are used, which leaves the registers for it.
+// The next block of a workgroup is loaded while the current one is encoded:
+// up to 8 bf16 workers its raw replica words and theta go to registers (the
+// block barriers wait for LDS traffic only), and pseudo-gradients are formed
+// from the raw words where they are used, which leaves the registers for it;
+// up to 8 fp32 workers its theta and replica vectors go straight to LDS
+// (global_load_lds_dwordx4, no registers), each wave into pieces only it reads
+// back, behind an explicit count of the vector memory instructions issued
+// after them (the compiler does not order these loads against later LDS
+// reads by itself).
 template <int K, int RT, bool STATS, bool RESET>
 __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr int NT = kInt8Threads;
@@ -142,9 +147,17 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr int G = 2;   // runs of W parameters per thread
     constexpr int W = V / G;
     constexpr bool PF = RT == RT_BF16 && K <= 8;
+    // fp32 replicas up to 8 workers: the next block's theta and replica vectors
+    // stream into LDS (direct global-to-LDS loads, no registers) while the
+    // current block is encoded; (K + 1) * 16 KB of LDS
+    constexpr bool LP = RT == RT_F32 && K <= 8;
+    constexpr int NW = NT / 64;
     constexpr int KW = RT == RT_BF16 ? K : 1;   // raw bf16 replica words held per thread
     __shared__ uint32_t lds_max[NT / 64 * K];   // worker block maxima
     __shared__ uint32_t lds_mmax[NT / 64];      // the mean's block maximum
+    // prefetched vectors, [stream (theta, replica 0..K-1)][run][wave][lane];
+    // every wave reads back only the 1 KB pieces it loaded itself
+    __shared__ f32x4 lds_pf[LP ? (K + 1) * G * NT : 1];
 
     double acc[NS];
 #pragma unroll
@@ -152,6 +165,24 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 
     const int64_t nfull = a.n / kCodecBlock;
     const int64_t nblocks = (a.n + kCodecBlock - 1) / kCodecBlock;
+
+    // LDS prefetch: this wave's piece of stream s, run g
+    const int wave = threadIdx.x >> 6;
+    auto pf_piece = [&](int s, int g) { return lds_pf + ((s * G + g) * NW + wave) * 64; };
+    // Issues the (K + 1) * G direct loads of full block b: lane l's 16 bytes
+    // land at its wave's piece + 16 l.
+    auto pf_issue = [&](int64_t b) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int64_t o = b * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W;
+#pragma unroll
+            for (int s = 0; s <= K; ++s) {
+                const float* src = s == 0 ? a.theta + o : static_cast<const float*>(a.replicas[s - 1]) + o;
+                __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                                 (void __attribute__((address_space(3)))*)pf_piece(s, g), 16, 0, 0);
+            }
+        }
+    };
 
     // bf16: raw words (two per run) and theta of one block (full: vector loads;
     // else per element, zero beyond n)
@@ -233,10 +264,36 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
             for (int e = 0; e < V; ++e) th[e] = cth[e];
         } else {
+            if constexpr (FULL && LP) {
+                // This block's direct loads were issued in the previous iteration
+                // (or before the loop), and every vector memory instruction issued
+                // after them is one of that iteration's stores: G of theta, G of
+                // v and, with the reset, G of each replica (more with the encoded
+                // mean).  In-order completion makes "at most that many
+                // outstanding" imply the loads have landed in LDS.
+                constexpr int after = G * (2 + (RESET ? K : 0));
+                __builtin_amdgcn_s_waitcnt((after & 0xF) | ((after >> 4) << 14) | 0x70 | 0xF00);
+            }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int64_t o = off[g];
-                if constexpr (FULL) {
+                if constexpr (FULL && LP) {
+                    // theta and the replicas from the LDS prefetch (complete: see the
+                    // wait at the end of the loop body), momentum from memory
+                    const int lane = threadIdx.x & 63;
+                    const f32x4 t4 = pf_piece(0, g)[lane], v4 = ld_f4(a.momentum + o);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        th[g * W + e] = t4[e];
+                        v[g * W + e] = v4[e];
+                    }
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const f32x4 r4 = pf_piece(k + 1, g)[lane];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) d[k][g * W + e] = th[g * W + e] - r4[e];
+                    }
+                } else if constexpr (FULL) {
                     const f32x4 t4 = ld_f4(a.theta + o), v4 = ld_f4(a.momentum + o);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -262,6 +319,14 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                     }
                 }
             }
+        }
+        if constexpr (RT == RT_F32 && LP && FULL) {
+            // every LDS read of this block has returned before the next block's
+            // direct loads overwrite the pieces; then issue them (on the last
+            // block of this workgroup, this block again, so every iteration
+            // issues the same instructions; those values are not used)
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            pf_issue(blk + gridDim.x < nfull ? blk + gridDim.x : blk);
         }
         // pseudo-gradient k of parameter e (bf16: from the raw replica word)
         auto D = [&](int k, int e) -> float {
@@ -430,6 +495,10 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         // entry (where they come from register moves), so the loop needs no wait
         // for them
         __builtin_amdgcn_s_waitcnt(0);
+    }
+    if constexpr (LP) {
+        if (blockIdx.x < nfull) pf_issue(blockIdx.x);
+        __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
     }
     for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{});
     // the shorter last block belongs to the workgroup the grid stride gives it
