@@ -501,6 +501,9 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
     }
     for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{});
+    // the last iteration's direct loads (a re-read, unused) land before anything
+    // else uses this workgroup's LDS or the workgroup ends
+    if constexpr (LP) __builtin_amdgcn_s_waitcnt(0);
     // the shorter last block belongs to the workgroup the grid stride gives it
     if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{});
 

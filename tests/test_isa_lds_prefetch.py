@@ -93,3 +93,10 @@ def test_prefetch_wait_covers_the_direct_loads(asm, st, rs):
         pro = [i for i in range(tail) if "global_load_lds" in body[i]]
         assert pro, (k, "no prologue prefetch")
         assert any("s_waitcnt vmcnt(0)" in body[i] for i in range(pro[-1], tail)), (k, "prologue not drained")
+        # after the loop (the code after its last branch back into the tail): a full wait
+        # comes before any LDS instruction and before the end of the program
+        close = max(back)
+        rest = body[close + 1:]
+        w = next((i for i, l in enumerate(rest) if "s_waitcnt vmcnt(0)" in l), None)
+        assert w is not None, (k, "no full wait after the loop")
+        assert not any(re.search(r"\bds_|s_endpgm", l) for l in rest[:w]), (k, "LDS used before the final wait")
