@@ -351,6 +351,36 @@ int blocks8(const autoloco_ctx* ctx, int64_t n) {
     return static_cast<int>(want < limit ? want : limit);
 }
 
+// Outer coefficients a kernel can use: finite, with rho > 0.
+int check_coeffs(autoloco_ctx* c, const autoloco_outer_coeffs* co) {
+    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
+        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    return AUTOLOCO_OK;
+}
+
+// Checks shared by the outer-step calls, in this order: buffers, coefficients
+// present, flags, the statistics output and eps (with FUSE_STATS), coefficient
+// values.  Sets *stats and *reset from the flags.
+int validate_step(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co, uint32_t flags,
+                  double eps, const autoloco_stats* out, bool* stats, bool* reset) {
+    int st = validate(c, b, true);
+    if (st != AUTOLOCO_OK) return st;
+    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
+    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
+    *stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
+    *reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
+    if (*stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
+    if (*stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    return check_coeffs(c, co);
+}
+
+// The corrected step's scalars in a round kernel's arguments (fp32; 1/rho when normalising).
+void set_step(RoundArgs& a, const autoloco_outer_coeffs* co) {
+    a.mu = static_cast<float>(co->mu);
+    a.eta = static_cast<float>(co->eta_out);
+    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+}
+
 void zero_stats(int k, double eps, autoloco_stats* out) {
     double z[kMaxSums] = {0};
     finish_stats(z, k, eps, out);
@@ -469,16 +499,9 @@ int autoloco_round_stats(autoloco_ctx* c, const autoloco_buffers* b, double eps,
 
 int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
                         uint32_t flags, double eps, autoloco_stats* out) {
-    int st = validate(c, b, true);
+    bool stats = false, reset = false;
+    const int st = validate_step(c, b, co, flags, eps, out, &stats, &reset);
     if (st != AUTOLOCO_OK) return st;
-    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
-    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
-    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
-    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
-    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
-    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
-    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
-        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
     if (b->n == 0) {
         if (stats) zero_stats(b->k, eps, out);
         return AUTOLOCO_OK;
@@ -486,9 +509,7 @@ int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autolo
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
-    a.mu = static_cast<float>(co->mu);
-    a.eta = static_cast<float>(co->eta_out);
-    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    set_step(a, co);
     const int mode = stats ? (reset ? MODE_UPDATE_STATS_RESET : MODE_UPDATE_STATS)
                            : (reset ? MODE_UPDATE_RESET : MODE_UPDATE);
     return run_round(c, b, a, mode, stats, eps, out);
@@ -496,16 +517,9 @@ int autoloco_outer_step(autoloco_ctx* c, const autoloco_buffers* b, const autolo
 
 int autoloco_outer_step_bf16(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
                              uint32_t flags, double eps, autoloco_stats* out, uint16_t* mean_bf16) {
-    int st = validate(c, b, true);
+    bool stats = false, reset = false;
+    const int st = validate_step(c, b, co, flags, eps, out, &stats, &reset);
     if (st != AUTOLOCO_OK) return st;
-    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
-    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
-    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
-    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
-    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
-    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
-    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
-        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
     if (b->n == 0) {
         if (stats) zero_stats(b->k, eps, out);
         return AUTOLOCO_OK;
@@ -528,9 +542,7 @@ int autoloco_outer_step_bf16(autoloco_ctx* c, const autoloco_buffers* b, const a
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
-    a.mu = static_cast<float>(co->mu);
-    a.eta = static_cast<float>(co->eta_out);
-    a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
+    set_step(a, co);
     a.payload = mean_bf16;
     a.inv_k64 = 1.0 / static_cast<double>(b->k);
     const int mode = stats ? (reset ? MODE_P_UPDATE_STATS_RESET : MODE_P_UPDATE_STATS)
@@ -540,16 +552,9 @@ int autoloco_outer_step_bf16(autoloco_ctx* c, const autoloco_buffers* b, const a
 
 int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
                              uint32_t flags, double eps, autoloco_stats* out, int8_t* codes, float* scales) {
-    int st = validate(c, b, true);
+    bool stats = false, reset = false;
+    const int st = validate_step(c, b, co, flags, eps, out, &stats, &reset);
     if (st != AUTOLOCO_OK) return st;
-    if (co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null coefficients");
-    if ((flags & ~(AUTOLOCO_FUSE_STATS | AUTOLOCO_FUSE_RESET)) != 0) return fail(c, AUTOLOCO_E_INVALID, "unknown flags");
-    const bool stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
-    const bool reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
-    if (stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
-    if (stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
-    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
-        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
     if ((codes == nullptr) != (scales == nullptr))
         return fail(c, AUTOLOCO_E_INVALID, "pass both payload buffers or neither");
     if (b->n == 0) {
@@ -767,8 +772,8 @@ int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const 
     if (b == nullptr || co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null buffers or coefficients");
     if (b->n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
     if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(c, AUTOLOCO_E_INVALID, "k outside 1..16");
-    if (!std::isfinite(co->mu) || !std::isfinite(co->eta_out) || !std::isfinite(co->rho) || !(co->rho > 0.0))
-        return fail(c, AUTOLOCO_E_INVALID, "coefficients must be finite with rho > 0");
+    const int cs = check_coeffs(c, co);
+    if (cs != AUTOLOCO_OK) return cs;
     if (b->n == 0) {
         if (sq_mean != nullptr) *sq_mean = 0.0;
         return AUTOLOCO_OK;
