@@ -358,14 +358,32 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
         block_max<K, NT>(amax, lds_max);
 
+        // The K scales and their reciprocals are the same in every lane: lane k
+        // computes worker k's (one IEEE division of each kind for all workers
+        // instead of K), and every lane reads them back.
+        float scale_k[K], recip_k[K];
+        {
+            const int lane = threadIdx.x & 63;
+            float am = amax[0];
+#pragma unroll
+            for (int k = 1; k < K; ++k) am = lane == k ? amax[k] : am;
+            const float sv = codec_scale(am);
+            const float rv = 1.0f / sv;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                scale_k[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv), k));
+                recip_k[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rv), k));
+            }
+        }
+
         // decode every worker and average: fp64 sum in worker order, times fp64(1/K)
         double sum[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) sum[e] = 0.0;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            const float s = codec_scale(amax[k]);
-            const float r = 1.0f / s;
+            const float s = scale_k[k];
+            const float r = recip_k[k];
             float q[V];
             codec_q<V>([&](int e) { return D(k, e); }, s, r, q);
 #pragma unroll
