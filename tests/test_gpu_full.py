@@ -146,3 +146,30 @@ def test_llama_1b1_full(ctx):
 
 def test_llama_3b_bf16_full(ctx):
     _large(ctx, "llama-3b", 8, torch.bfloat16, parts=64, oracle_parts=[17, 63], normalize=True)
+
+
+def test_llama_1b1_interval_ratios(ctx):
+    # the 1.1B configuration's selected/base interval ratios 0.5, 1, 1.5, 2 (H^ref = 500
+    # from step 20,000): rho = 1, 1, 1.4914, 1.9771, each round on freshly drawn replicas,
+    # with and without normalisation
+    n, k = shapes.llama_1b1().n_params, 8
+    ts, _ = al.spread_tensors(ctx, n, [torch.float32] * (k + 2))
+    inp = drift.RoundInputs(ts[0], ts[1], ts[2:])
+    drift.fill_theta_momentum(inp, seed=42)
+    idx = _sample_index(n, m=1 << 18, seed=4)
+    rhos = []
+    for i, (h_sel, normalize) in enumerate([(250, False), (500, True), (750, True), (1000, False)]):
+        drift.fill_replicas(inp, seed=60 + i)
+        c = _coeffs(h_sel=h_sel, normalize=normalize)
+        rhos.append(c.rho)
+        sample_in = _gather(inp, idx)
+        print(f"1.1B ratio {h_sel / 500}: rho {c.rho:.6f} normalise {normalize}", flush=True)
+        st = al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, c, al.FUSE_STATS | al.FUSE_RESET,
+                                    EPS)
+        torch.cuda.synchronize()
+        assert st.finite and st.disagreement == pytest.approx(st.D - st.sq_mean, rel=1e-4)
+        _check_sampled_outputs(inp, idx, sample_in, c, torch.float32)
+    assert rhos[0] == 1.0 and rhos[1] == 1.0
+    assert rhos[2] == pytest.approx(1.491439580, rel=1e-9) and rhos[3] == pytest.approx(1.977132131, rel=1e-9)
+    del inp, ts
+    torch.cuda.empty_cache()
