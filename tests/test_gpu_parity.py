@@ -210,10 +210,10 @@ def test_grid_size_changes_only_rounding(ctx):
         al.autoloco_set_grid_limit(ctx, 0)
 
 
-def test_largest_grid(ctx):
+@pytest.mark.parametrize("n,k", [(17_000_003, 9), (67_200_003, 2)])
+def test_largest_grid(ctx, n, k):
     # 16,384 workgroups (the scratch capacity): every partial slot in use, and the
     # finishing kernel's strided loop runs 64 times per thread
-    n, k = 17_000_003, 4
     inp = cpu_inputs(n, k, seed=19)
     dev = to_device(inp)
     c = _tiny_coeffs(True)
