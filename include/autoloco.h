@@ -119,7 +119,10 @@ int autoloco_launch_shape(const autoloco_ctx* ctx, int64_t n, int32_t k, int32_t
  * which.  Each buffer is freed with autoloco_free.
  * Errors: E_INVALID (null pointers, count outside 1..64, bytes == 0), E_NOMEM. */
 int autoloco_alloc_spread(autoloco_ctx* ctx, int32_t count, size_t bytes, void** out, int32_t* spread);
-/* Frees one buffer from autoloco_alloc_spread (NULL is a no-op). */
+/* Frees one buffer from autoloco_alloc_spread (NULL is a no-op).  The buffers
+ * are not owned by the context that made them: destroying it frees none of
+ * them, and any context of the same device may free them.
+ * Errors: E_INVALID (null context), E_DEVICE (hipFree failed). */
 int autoloco_free(autoloco_ctx* ctx, void* ptr);
 
 /* ------------------------------------------------------------------------ */

@@ -207,11 +207,25 @@ class Context:
         _check(lib().autoloco_create(device, C.c_void_p(raw), C.byref(h)), "autoloco_create")
         self.handle = h
         self.device = device
+        # spread buffers not yet freed; while there are any, close() detaches the
+        # handle from the API but keeps the native context for their frees
+        self._live = 0
+        self._held = None
 
     def close(self):
-        if getattr(self, "handle", None):
-            lib().autoloco_destroy(self.handle)
+        h = getattr(self, "handle", None)
+        if h:
             self.handle = None
+            if self._live:
+                self._held = h
+            else:
+                lib().autoloco_destroy(h)
+
+    def _buffer_freed(self):
+        self._live -= 1
+        if self._live == 0 and self._held is not None:
+            h, self._held = self._held, None
+            lib().autoloco_destroy(h)
 
     def __del__(self):
         try:
@@ -271,6 +285,7 @@ class _DeviceBuffer:
         self._ctx = ctx
         self.ptr = ptr
         self.nbytes = nbytes
+        ctx._live += 1
 
     def view(self, n: int, dtype):
         import torch
@@ -290,12 +305,17 @@ class _DeviceBuffer:
         raise TypeError(dtype)
 
     def __del__(self):
+        ptr, self.ptr = self.ptr, 0
+        if not ptr:
+            return
+        ctx = self._ctx
         try:
-            if self.ptr and self._ctx.handle:
-                lib().autoloco_free(self._ctx.handle, C.c_void_p(self.ptr))
+            h = ctx.handle or ctx._held
+            if h:
+                lib().autoloco_free(h, C.c_void_p(ptr))
         except Exception:
             pass
-        self.ptr = 0
+        ctx._buffer_freed()
 
 
 def autoloco_alloc_spread(ctx: "Context", count: int, nbytes: int):

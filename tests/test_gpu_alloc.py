@@ -63,3 +63,32 @@ def test_alloc_spread_rejects_bad_arguments(ctx):
     assert al.lib().autoloco_alloc_spread(ctx.handle, 2, 0, out, None) == -1
     assert al.lib().autoloco_alloc_spread(ctx.handle, 2, 1024, None, None) == -1
     assert al.lib().autoloco_free(ctx.handle, None) == 0
+
+
+def test_buffers_outliving_their_context_are_freed():
+    # closing the context while its spread buffers are still alive detaches it
+    # from the API at once; the buffers keep their memory until they are
+    # collected and then return it (the native context goes with the last one)
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info(0)
+    c = al.autoloco_create(0)
+    n = 256 << 20   # 1 GiB per fp32 buffer
+    ts, _ = al.spread_tensors(c, n, [torch.float32] * 2)
+    ts[0].fill_(1.5)
+    ts[1].copy_(ts[0])
+    c.close()
+    assert c.handle is None
+    with pytest.raises(Exception):
+        al.autoloco_launch_shape(c, 1024, 2)
+    # still this process's memory after the close
+    assert [float(ts[1][i]) for i in (0, n // 2, n - 1)] == [1.5] * 3
+    held, _ = torch.cuda.mem_get_info(0)
+    assert free0 - held >= 2 * (n * 4)
+    del ts
+    gc.collect()
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info(0)
+    assert c._held is None and c._live == 0
+    assert free1 >= free0 - (64 << 20), (free0, free1)
