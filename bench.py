@@ -44,6 +44,21 @@ WORKLOADS = {
 }
 
 
+_LABEL = {"llama-1.1b": "1.1B params", "gpt2-small": "124M params (GPT-2 small)", "llama-3b-bf16": "3B params",
+          "llama-7b": "7B params", "tiny": "1M params"}
+
+
+def metric_name(base: str, args, k: int, steps_tail: bool = False) -> str:
+    """The metric string: `base` names its headline workload after the last
+    comma; another workload or K replaces that part with its own."""
+    head, _, tail = base.rpartition(", ")
+    own = f"{_LABEL[args.workload]} K={k}" + (f", {args.steps} rounds" if steps_tail else "")
+    if steps_tail:
+        head, _, mid = head.rpartition(", ")
+        tail = f"{mid}, {tail}"
+    return base if tail == own else f"{head}, {own}"
+
+
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -292,7 +307,7 @@ def bench_inner(args) -> int:
             leg["gpu_speedup"] = (n * k / (ms_per_step * 1e-3)) / leg["value"]
 
     out = {
-        "metric": INNER_METRIC,
+        "metric": metric_name(INNER_METRIC, args, k),
         "value": n * k / (ms_per_step * 1e-3),
         "unit": "worker-params/s",
         "n_gpus": 1,
@@ -531,7 +546,7 @@ def bench_closed_loop(args) -> int:
         cpu["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / cpu["value"]
     tag = f"round_{rdt}_k{k}_{args.workload}"
     out = {
-        "metric": CLOSED_LOOP_METRIC,
+        "metric": metric_name(CLOSED_LOOP_METRIC, args, k, steps_tail=True),
         "value": n / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,
@@ -747,7 +762,7 @@ def main() -> int:
             leg["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / leg["value"]
 
     out = {
-        "metric": METRIC,
+        "metric": metric_name(METRIC, args, k),
         "value": n / (ms_per_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,

@@ -41,6 +41,7 @@ def test_round_line():
               "--cpu-sample", str(1 << 16)])
     _common(d, 3, 1)
     assert d["unit"] == "params/s" and d["config"]["n_params"] == 1 << 20
+    assert d["metric"].endswith(", 1M params K=4")
     assert d["value"] == pytest.approx(d["config"]["n_params"] / (d["ms_per_step"] * 1e-3), rel=1e-9)
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["unit"] == "params/s"
@@ -54,3 +55,4 @@ def test_closed_loop_line():
     d = _run(["--step", "closed-loop", "--workload", "tiny", "--steps", "4", "--warmup", "1", "--no-cpu-baseline"])
     _common(d, 4, 1)
     assert len(d["rounds"]) == 5 and all(r["h_step"] > 0 for r in d["rounds"])
+    assert d["metric"].endswith(", 1M params K=4, 4 rounds")
