@@ -59,6 +59,13 @@ def metric_name(base: str, args, k: int, steps_tail: bool = False) -> str:
     return base if tail == own else f"{head}, {own}"
 
 
+def alloc_label(alloc: str, spread: bool) -> str:
+    """How the streamed buffers were placed."""
+    if alloc != "spread":
+        return "torch"
+    return "spread" if spread else "spread requested, plain (too little free memory)"
+
+
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -324,7 +331,7 @@ def bench_inner(args) -> int:
                         f"parameters, moments and gradients, per-worker gradient-norm clipping 1.0, "
                         f"betas (0.9, 0.95), weight decay 0.1" + (", BF16 compute copy" if args.copy else ""),
             "n_params": n, "k": k, "update_bytes": update_bytes, "norm_bytes": norm_bytes,
-            "alloc": args.alloc + (" (spread)" if spread else ""),
+            "alloc": alloc_label(args.alloc, spread),
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -440,7 +447,7 @@ def bench_share(args) -> int:
                         f"{rdt} replica, BF16 payloads; shard of {ns:,} parameters; collectives not run",
             "n_params": n, "k": k, "shard": ns, "bytes": {"payload": b_payload, "shard_step": b_shard,
                                                           "reset": b_reset},
-            "alloc": "spread" if spread else "spread (not spread)",
+            "alloc": alloc_label("spread", spread),
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -563,7 +570,7 @@ def bench_closed_loop(args) -> int:
                         f"Nesterov + reset with the coefficients the interval controller chose, the controller "
                         f"fed each round's statistics (C4 settings, budget 50,000 steps)",
             "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
-            "alloc": "spread" if spread else "plain", "fault_round": next((t["round"] for t in trace if t["fault"]), None),
+            "alloc": alloc_label("spread", spread), "fault_round": next((t["round"] for t in trace if t["fault"]), None),
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -780,7 +787,7 @@ def main() -> int:
                         + {"fp32": "", "int8": ", worker average through the INT8 blockwise codec",
                            "bf16": ", worker average as BF16 pseudo-gradient payloads"}[args.codec],
             "n_params": n, "k": k, "replica_dtype": rdt, "bytes_per_round": bytes_per_round,
-            "grid": [blocks, threads] if args.codec == "fp32" else None, "alloc": args.alloc + (" (spread)" if spread else ""),
+            "grid": [blocks, threads] if args.codec == "fp32" else None, "alloc": alloc_label(args.alloc, spread),
             "codec": args.codec + (" + payload" if codes is not None else ""),
             "h_selected": h_sel, "h_base": h_base,
             "rho": coeffs.rho, "mu": coeffs.mu, "eta_out": coeffs.eta_out,
