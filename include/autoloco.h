@@ -88,7 +88,10 @@ const char* autoloco_last_error(const autoloco_ctx* ctx);
  * that autoloco_last_kernel_ms() can report the device time of the most recent
  * call.  Off by default. */
 int autoloco_set_timing(autoloco_ctx* ctx, int enable);
-/* Device milliseconds of the last timed launch; waits for it to finish. */
+/* Device milliseconds of the last timed launch; waits for it to finish.
+ * Errors: E_INVALID (null argument), E_STATE (timing off, no timed launch yet,
+ * or the last call that launched device work failed after it began),
+ * E_DEVICE. */
 int autoloco_last_kernel_ms(autoloco_ctx* ctx, float* ms);
 /* Cap on the number of workgroups of the streaming kernels, 0..16384 (0 = the
  * default: three workgroups per compute unit, or fewer if the fused kernel's

@@ -212,24 +212,40 @@ RoundArgs make_args(autoloco_ctx* ctx, const autoloco_buffers* b) {
     return a;
 }
 
+// Timing of a call's device work.  The previous timing is dropped before the
+// start event of a new launch is recorded, so a call that fails after that
+// point leaves no timing (E_STATE) rather than a start and stop of two calls.
+int timer_start(autoloco_ctx* c) {
+    c->timed_valid = false;
+    if (!c->timing) return AUTOLOCO_OK;
+    const hipError_t e = hipEventRecord(c->ev_start, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    return AUTOLOCO_OK;
+}
+
+int timer_stop(autoloco_ctx* c, bool adamw = false, bool norm_ran = false) {
+    if (!c->timing) return AUTOLOCO_OK;
+    const hipError_t e = hipEventRecord(c->ev_stop, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventRecord");
+    c->timed_valid = true;
+    c->adamw_timed = adamw;
+    c->adamw_norm_ran = norm_ran;
+    return AUTOLOCO_OK;
+}
+
 // Launches one round kernel (timed if requested); with stats, waits for the
 // sums and fills *out.
 int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, int mode, bool stats,
               double eps, autoloco_stats* out) {
     const int blocks = blocks_for(ctx, b->n, b->replica_dtype, b->k, mode >= MODE_P_UPDATE);
-    hipError_t e;
-    if (ctx->timing && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
-    e = launcher(b->replica_dtype, mode)(b->k, blocks, ctx->stream, a);
+    int ts = timer_start(ctx);
+    if (ts != AUTOLOCO_OK) return ts;
+    hipError_t e = launcher(b->replica_dtype, mode)(b->k, blocks, ctx->stream, a);
     if (e != hipSuccess) return hip_fail(ctx, e, "kernel launch");
     if (stats && (e = launch_finish_sums(2 * b->k + 1, kBlock, blocks, ctx->partials, ctx->sums, ctx->stream)) !=
                      hipSuccess)
         return hip_fail(ctx, e, "reduction launch");
-    if (ctx->timing) {
-        if ((e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
-        ctx->timed_valid = true;
-        ctx->adamw_timed = false;
-    }
+    if ((ts = timer_stop(ctx)) != AUTOLOCO_OK) return ts;
     if (stats) {
         const size_t bytes = sizeof(double) * (2 * b->k + 1);
         e = hipMemcpyAsync(ctx->host_sums, ctx->sums, bytes, hipMemcpyDeviceToHost, ctx->stream);
@@ -320,16 +336,13 @@ int check_ranges(autoloco_ctx* ctx, const std::vector<Range>& r) {
 // waits for it and stores it.
 template <typename Launch>
 int run_one_sum(autoloco_ctx* c, Launch launch, int blocks, double* out) {
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
     hipError_t e;
-    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     if ((e = launch()) != hipSuccess) return hip_fail(c, e, "kernel launch");
     if ((e = launch_finish_sums(1, kBlock, blocks, c->partials, c->sums, c->stream)) != hipSuccess)
         return hip_fail(c, e, "reduction launch");
-    if (c->timing) {
-        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-        c->timed_valid = true;
-        c->adamw_timed = false;
-    }
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     if (out != nullptr) {
         if ((e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double), hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
             return hip_fail(c, e, "hipMemcpyAsync");
@@ -608,18 +621,14 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
     static const Int8Launcher table[2][2][2] = {
         {{launch_int8_f32_s0r0, launch_int8_f32_s0r1}, {launch_int8_f32_s1r0, launch_int8_f32_s1r1}},
         {{launch_int8_bf16_s0r0, launch_int8_bf16_s0r1}, {launch_int8_bf16_s1r0, launch_int8_bf16_s1r1}}};
-    hipError_t e;
-    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-    e = table[rt][stats ? 1 : 0][reset ? 1 : 0](b->k, blocks, c->stream, a);
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
+    hipError_t e = table[rt][stats ? 1 : 0][reset ? 1 : 0](b->k, blocks, c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
     if (stats && (e = launch_finish_sums(2 * b->k + 1, kInt8Threads, blocks, c->partials, c->sums, c->stream)) !=
                      hipSuccess)
         return hip_fail(c, e, "reduction launch");
-    if (c->timing) {
-        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-        c->timed_valid = true;
-        c->adamw_timed = false;
-    }
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     if (stats) {
         const size_t bytes = sizeof(double) * (2 * b->k + 1);
         e = hipMemcpyAsync(c->host_sums, c->sums, bytes, hipMemcpyDeviceToHost, c->stream);
@@ -640,15 +649,11 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
     const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k);
-    hipError_t e;
-    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-    e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
+    hipError_t e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
-    if (c->timing) {
-        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-        c->timed_valid = true;
-        c->adamw_timed = false;
-    }
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     c->err.clear();
     return AUTOLOCO_OK;
 }
@@ -661,15 +666,11 @@ int autoloco_traffic_reference(autoloco_ctx* c, const autoloco_buffers* b) {
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
     const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k);
-    hipError_t e;
-    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-    e = launch_traffic(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a, 0u);
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
+    hipError_t e = launch_traffic(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a, 0u);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
-    if (c->timing) {
-        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-        c->timed_valid = true;
-        c->adamw_timed = false;
-    }
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     c->err.clear();
     return AUTOLOCO_OK;
 }
@@ -833,8 +834,9 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     const bool norm_pass = clip || out != nullptr;
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
     hipError_t e;
-    if (c->timing && (e = hipEventRecord(c->ev_start, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
     if (norm_pass) {
         GradNormArgs na;
         std::memset(&na, 0, sizeof(na));
@@ -871,12 +873,7 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
     a.eps = static_cast<float>(co->eps);
     e = launch_adamw(copy, b->k, adamw_blocks(c, b->n, b->k), c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "AdamW launch");
-    if (c->timing) {
-        if ((e = hipEventRecord(c->ev_stop, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
-        c->timed_valid = true;
-        c->adamw_timed = true;
-        c->adamw_norm_ran = norm_pass;
-    }
+    if ((ts = timer_stop(c, true, norm_pass)) != AUTOLOCO_OK) return ts;
     if (out != nullptr) {
         e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double) * b->k, hipMemcpyDeviceToHost, c->stream);
         if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync");

@@ -362,12 +362,28 @@ def test_rejects_host_memory(ctx):
 
 
 def test_timing_events(ctx):
+    E_STATE = -6   # AUTOLOCO_E_STATE
     inp = to_device(cpu_inputs(1 << 20, 4, seed=43))
     al.autoloco_set_timing(ctx, True)
     try:
+        with pytest.raises(al.AutolocoError) as ei:   # nothing timed yet
+            al.autoloco_last_kernel_ms(ctx)
+        assert ei.value.status == E_STATE
         al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, _tiny_coeffs(False),
                                al.FUSE_STATS | al.FUSE_RESET, EPS)
         ms = al.autoloco_last_kernel_ms(ctx)
         assert 0.0 < ms < 100.0
+        # a call refused before launching anything leaves the last timing in place
+        with pytest.raises(al.AutolocoError):
+            al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, _tiny_coeffs(False), 8, EPS)
+        assert al.autoloco_last_kernel_ms(ctx) == ms
+        with pytest.raises(al.AutolocoError) as ei:   # the last timed call was no AdamW step
+            al.autoloco_last_adamw_ms(ctx)
+        assert ei.value.status == E_STATE
+        al.autoloco_broadcast_reset(ctx, inp.theta, inp.replicas)
+        assert 0.0 < al.autoloco_last_kernel_ms(ctx) < 100.0
     finally:
         al.autoloco_set_timing(ctx, False)
+    with pytest.raises(al.AutolocoError) as ei:   # switching timing off drops it
+        al.autoloco_last_kernel_ms(ctx)
+    assert ei.value.status == E_STATE
