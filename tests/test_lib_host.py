@@ -19,7 +19,8 @@ HEADER = os.path.join(ROOT, "include", "autoloco.h")
 
 
 def _declared_functions():
-    text = open(HEADER).read()
+    with open(HEADER) as f:
+        text = f.read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"^[A-Za-z_][\w \*]*?\b(autoloco_\w+)\s*\(", text, flags=re.M)))
 
