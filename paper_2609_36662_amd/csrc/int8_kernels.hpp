@@ -49,31 +49,45 @@ __device__ __forceinline__ float codec_scale(float amax) {
 
 // Codes of x[0..NV) at scale s (r = fp32(1/s)): the integers nearest
 // fp32(x / s), ties to even, clipped to +-127.  t = x * r differs from
-// fp32(x / s) by at most 1.5 * 2^-23 * |x / s| <= 2.3e-5 here (|x / s| <= 127),
-// so rint(t) is the same integer unless t lies within that distance of a
-// half-integer; only then (about 1e-4 of the elements) is the IEEE quotient
+// fp32(x / s) by at most (3u + u^2) |x / s| <= 2.28e-5 here (u = 2^-24,
+// |x / s| <= 127.00003; the test's own rounding, fused or not, adds at most
+// 3e-8), so rint(t) is the same integer unless t lies within 3e-5 of a
+// half-integer; only then (about 6e-5 of the elements) is the IEEE quotient
 // formed.  The test runs for every element first and the quotients are taken
 // behind one wavefront-uniform branch, entered only when some lane of the
 // wavefront needs one, so the common path has no per-element branch.
+// The clip is implied by the scale and costs no instruction: s is the block's
+// largest magnitude over 127 rounded once (or the larger 2^-126), so |t| and
+// |fp32(x / s)| are at most 127 (1 + 3 * 2^-24) < 127.5 for every x of the
+// block, and their nearest integers lie in [-127, 127].  (A non-finite block
+// has a NaN or infinite scale and decodes to non-finite values either way.)
 // x(e) gives element e (evaluated again on the rare path).
 template <int NV, typename X>
 __device__ __forceinline__ void codec_q(X x, float s, float r, float (&q)[NV]) {
-    bool bad[NV];
+    // t may lie too close to a half-integer (also true for NaN)
+    auto near_half = [](float t, float qi) { return !(fabsf(t - qi) < 0.5f - 3.0e-5f); };
     bool any = false;
 #pragma unroll
     for (int e = 0; e < NV; ++e) {
         const float t = x(e) * r;
         q[e] = __builtin_rintf(t);
-        bad[e] = !(fabsf(t - q[e]) < 0.5f - 6.0e-5f);   // also true for NaN
-        any = any || bad[e];
+        any = any || near_half(t, q[e]);
     }
     if (__builtin_amdgcn_ballot_w64(any) != 0) {
 #pragma unroll
         for (int e = 0; e < NV; ++e)
-            if (bad[e]) q[e] = __builtin_rintf(x(e) / s);
+            if (near_half(x(e) * r, q[e])) q[e] = __builtin_rintf(x(e) / s);
     }
-#pragma unroll
-    for (int e = 0; e < NV; ++e) q[e] = __builtin_amdgcn_fmed3f(q[e], -127.0f, 127.0f);   // clip to [-127, 127]
+}
+
+// fp32 -> bf16 of a pair, round to nearest even, in one gfx950 conversion
+// instruction.  For every input other than NaN it gives the same bits as
+// bf16_rne (checked on MI355X over all 2^32 patterns); a NaN stays a quiet NaN
+// and keeps the top bits of its payload instead of becoming the canonical one.
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Maximum over the 64 lanes of a wavefront of a non-negative float (or NaN),
@@ -186,8 +200,10 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 
     // bf16: raw words (two per run) and theta of one block (full: vector loads;
     // else per element, zero beyond n)
-    u32x2 cw[KW][G];
-    float cth[V];
+    // two register sets for the bf16 prefetch: the loop takes blocks in pairs and
+    // the sets swap roles (current / next) instead of being copied
+    u32x2 wA[KW][G], wB[PF ? KW : 1][G];
+    float tA[V], tB[PF ? V : 1];
     auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto full_c) {
         constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
@@ -217,7 +233,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
     };
 
-    auto body = [&](int64_t blk, auto full_c) {
+    auto body = [&](int64_t blk, auto full_c, auto& cw, auto& cth, auto& nw, auto& nth) {
         constexpr bool FULL = decltype(full_c)::value;
         int64_t off[G];
         int valid[G];
@@ -236,8 +252,6 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
 
         float th[V], v[V], d[RT == RT_F32 ? K : 1][V];
-        u32x2 nw[PF ? K : 1][G];
-        float nth[V];
         if constexpr (RT == RT_BF16) {
             // momentum first: the update waits for it, and in-order completion
             // then leaves the prefetch below in flight
@@ -471,7 +485,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
                         for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + o, t4);
                     } else {
-                        const u32x2 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3])};
+                        const u32x2 w = {bf16_pair(tn[0], tn[1]), bf16_pair(tn[2], tn[3])};
 #pragma unroll
                         for (int k = 0; k < K; ++k)
                             __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.replicas[k]) + o));
@@ -496,34 +510,30 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 }
             }
         }
-        if constexpr (PF && FULL) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                cw[k][0] = nw[k][0];
-                cw[k][1] = nw[k][1];
-            }
-#pragma unroll
-            for (int e = 0; e < V; ++e) cth[e] = nth[e];
-        }
     };
 
     if constexpr (PF) {
-        if (blockIdx.x < nfull) load_bf16(blockIdx.x, cw, cth, BoolC<true>{});
-        // the first block's words are complete before the loop, as on every later
-        // entry (where they come from register moves), so the loop needs no wait
-        // for them
+        if (blockIdx.x < nfull) load_bf16(blockIdx.x, wA, tA, BoolC<true>{});
+        // the first block's words are complete before the loop
         __builtin_amdgcn_s_waitcnt(0);
+        // blocks in pairs: the first of a pair prefetches into B, the second into A
+        for (int64_t blk = blockIdx.x; blk < nfull; blk += 2 * (int64_t)gridDim.x) {
+            body(blk, BoolC<true>{}, wA, tA, wB, tB);
+            if (blk + gridDim.x >= nfull) break;
+            body(blk + gridDim.x, BoolC<true>{}, wB, tB, wA, tA);
+        }
+    } else {
+        if constexpr (LP) {
+            if (blockIdx.x < nfull) pf_issue(blockIdx.x);
+            __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
+        }
+        for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{}, wA, tA, wB, tB);
+        // the last iteration's direct loads (a re-read, unused) land before anything
+        // else uses this workgroup's LDS or the workgroup ends
+        if constexpr (LP) __builtin_amdgcn_s_waitcnt(0);
     }
-    if constexpr (LP) {
-        if (blockIdx.x < nfull) pf_issue(blockIdx.x);
-        __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
-    }
-    for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{});
-    // the last iteration's direct loads (a re-read, unused) land before anything
-    // else uses this workgroup's LDS or the workgroup ends
-    if constexpr (LP) __builtin_amdgcn_s_waitcnt(0);
     // the shorter last block belongs to the workgroup the grid stride gives it
-    if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{});
+    if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{}, wA, tA, wB, tB);
 
     if constexpr (STATS) store_partials<NS, NT>(acc, a.partials);
 }

@@ -179,3 +179,31 @@ def test_llama_1b1_sampled_codec_blocks(ctx):
 
 def test_llama_3b_bf16_sampled_codec_blocks(ctx):
     _sampled_codec_blocks(ctx, "llama-3b", 8, torch.bfloat16, True, seed=5)
+
+
+@pytest.mark.parametrize("dtype,k", [(torch.float32, 1), (torch.float32, 3), (torch.bfloat16, 2)])
+def test_codes_at_rounding_boundaries(ctx, dtype, k):
+    # theta holds blocks crowded at the tie points of their own scale (and next
+    # to them), the replicas are zero, so every worker's pseudo-gradient is
+    # exactly theta and its codes are decided at those boundaries; the last block
+    # is ragged.  Codes and scales of the encoded mean must equal the oracle's.
+    from tests.int8_cases import near_half_block
+    rng = np.random.default_rng(17)
+    amaxes = (1.0, 3.7, 0.3)
+    n = 3 * 4096 - 1000
+    theta = np.concatenate([near_half_block(a, min(4096, n - 4096 * i), rng) for i, a in enumerate(amaxes)])
+    momentum = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    inp = drift.RoundInputs(torch.from_numpy(theta), torch.from_numpy(momentum),
+                            [torch.zeros(n, dtype=dtype) for _ in range(k)])
+    dev = to_device(inp)
+    c = al.make_coeffs(COEFFS["mu"], COEFFS["eta_out"], COEFFS["rho"], True)
+    ref = ic.int8_round(theta, momentum, [host_array(r) for r in inp.replicas], c.mu, c.eta_out, c.rho, True, EPS)
+    codes, scales = _payload(n)
+    st = al.autoloco_outer_step_int8(ctx, dev.theta, dev.momentum, dev.replicas, c, al.FUSE_STATS | al.FUSE_RESET,
+                                     EPS, mean_codes=codes, mean_scales=scales)
+    torch.cuda.synchronize()
+    assert np.array_equal(codes[:n].cpu().numpy(), ref.mean_codes), "mean codes differ"
+    assert np.array_equal(scales[:3].cpu().numpy().view(np.uint32), ref.mean_scales.view(np.uint32)), "scales differ"
+    assert_stats_close(st, ref.stats, floor=1e-9 * max(ref.stats.D, 1e-30))
+    assert_close_elementwise(dev.theta.cpu().numpy(), ref.theta, what="theta'")
+    assert_close_elementwise(dev.momentum.cpu().numpy(), ref.momentum, what="v'")

@@ -131,3 +131,23 @@ def test_dyadic_round_equals_exact_rational(seed):
         assert float(s) == float(np.float32(float(s)))         # still exact in FP32
         agg += [max(-127, min(127, _round_half_even(v / s))) * s for v in seg]
     assert [float(a) for a in agg] == r.mean_decoded.astype(np.float64).tolist()
+
+
+def test_near_half_cases_need_the_exact_quotient():
+    # The GPU parity cases of tests/int8_cases.py are only a test of the codec's
+    # exact path if the product with the rounded reciprocal gives a different
+    # code than the paper's division for some of them: count those.
+    from tests.int8_cases import block_scale, near_half_block
+    rng = np.random.default_rng(11)
+    differ = ties = 0
+    for amax in (1.0, 3.7, 0.3, 2.0 ** -100 * 5.0):
+        x = near_half_block(amax, 4096, rng)
+        s = block_scale(amax)
+        codes, scales = ic.encode(x)
+        assert scales[0] == s and np.max(np.abs(x)) == np.float32(amax)
+        fast = np.clip(np.rint(x * (np.float32(1.0) / s)), -127, 127).astype(np.int8)
+        differ += int(np.sum(fast != codes))
+        qf = x / s                                 # the FP32 quotient the codes are defined on
+        ties += int(np.sum(qf - np.floor(qf) == np.float32(0.5)))
+    assert differ > 0, "no case where the product and the quotient round apart"
+    assert ties > 0, "no FP32 quotient on a tie, where rounding to even decides"
