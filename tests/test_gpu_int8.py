@@ -207,3 +207,17 @@ def test_codes_at_rounding_boundaries(ctx, dtype, k):
     assert_stats_close(st, ref.stats, floor=1e-9 * max(ref.stats.D, 1e-30))
     assert_close_elementwise(dev.theta.cpu().numpy(), ref.theta, what="theta'")
     assert_close_elementwise(dev.momentum.cpu().numpy(), ref.momentum, what="v'")
+
+
+@pytest.mark.parametrize("grid", [1, 2, 3])
+@pytest.mark.parametrize("dtype,k", [(torch.bfloat16, 8), (torch.bfloat16, 16), (torch.float32, 8)])
+def test_many_blocks_per_workgroup(ctx, grid, dtype, k):
+    # a capped grid gives every workgroup several codec blocks, even and odd
+    # counts, so the prefetching loops go round (bf16 up to K = 8: blocks in pairs
+    # with the two register sets swapping roles; fp32 up to K = 8: the LDS
+    # prefetch) and the ragged last block follows them
+    al.autoloco_set_grid_limit(ctx, grid)
+    try:
+        _check(ctx, 7 * 4096 + 100, k, dtype=dtype, seed=50 + grid + k, normalize=grid % 2 == 1)
+    finally:
+        al.autoloco_set_grid_limit(ctx, 0)
