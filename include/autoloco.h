@@ -34,7 +34,9 @@
  *   - Device buffers are flat, contiguous arrays of n elements, 16-byte
  *     aligned, and must not overlap one another.
  *   - Non-finite values in the data are not an error: they propagate through
- *     the update and are reported as finite = 0 in the statistics.
+ *     the update and are reported as finite = 0 in the statistics.  Values
+ *     narrowed to bf16 round to nearest, ties to even; a NaN stays a quiet
+ *     NaN (its payload bits are not specified).
  */
 #ifndef AUTOLOCO_H
 #define AUTOLOCO_H
@@ -206,9 +208,7 @@ int autoloco_outer_step(autoloco_ctx* ctx, const autoloco_buffers* bufs,
  * last one is shorter.  mean_codes ([n] int8) and mean_scales
  * ([ceil(n / 4096)] fp32) receive the encoded mean, the payload every worker
  * would receive; pass both or neither (NULL).  Non-finite data propagates and
- * is reported as finite = 0; the codes of such blocks are unspecified, and a
- * NaN written to a bf16 replica by the reset is a quiet NaN whose payload is
- * not specified.
+ * is reported as finite = 0; the codes of such blocks are unspecified.
  * Errors: as autoloco_outer_step, plus E_INVALID for only one payload buffer,
  * E_ALIGN / E_ALIAS for the payload buffers. */
 int autoloco_outer_step_int8(autoloco_ctx* ctx, const autoloco_buffers* bufs,

@@ -80,16 +80,6 @@ __device__ __forceinline__ void codec_q(X x, float s, float r, float (&q)[NV]) {
     }
 }
 
-// fp32 -> bf16 of a pair, round to nearest even, in one gfx950 conversion
-// instruction.  For every input other than NaN it gives the same bits as
-// bf16_rne (checked on MI355X over all 2^32 patterns); a NaN stays a quiet NaN
-// and keeps the top bits of its payload instead of becoming the canonical one.
-__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
-}
-
 // Maximum over the 64 lanes of a wavefront of a non-negative float (or NaN),
 // compared as its bit pattern, which orders non-negative floats as numbers:
 // DPP exchanges within each row of 16 lanes, then the four row results are read
@@ -485,7 +475,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 #pragma unroll
                         for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + o, t4);
                     } else {
-                        const u32x2 w = {bf16_pair(tn[0], tn[1]), bf16_pair(tn[2], tn[3])};
+                        const u32x2 w = {bf16_pack(tn[0], tn[1]), bf16_pack(tn[2], tn[3])};
 #pragma unroll
                         for (int k = 0; k < K; ++k)
                             __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.replicas[k]) + o));

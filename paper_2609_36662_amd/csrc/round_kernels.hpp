@@ -91,18 +91,20 @@ __device__ __forceinline__ void st_u2_at(void* base, uint32_t off, u32x2r v) {
     __builtin_nontemporal_store(v, reinterpret_cast<u32x2r*>(static_cast<char*>(base) + off));
 }
 
-// bf16 <-> fp32.  Widening is exact; narrowing rounds to nearest, ties to
-// even, keeps infinities and turns every NaN into the quiet NaN 0x7FC0 with
-// its sign.
+// bf16 <-> fp32.  Widening is exact.  Narrowing is gfx950's conversion
+// instruction (one for a pair): round to nearest, ties to even, subnormals and
+// infinities kept, overflow to infinity; a NaN stays a quiet NaN with the top
+// of its payload.  (Over all 2^32 inputs other than NaN it gives the bits of
+// the integer formulation (u + 0x7FFF + lsb) >> 16, checked on MI355X.)
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ __forceinline__ uint32_t bf16_rne(float x) {
-    const uint32_t u = __float_as_uint(x);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) & 0x8000u) | 0x7fc0u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
 __device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
-    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x));
 }
 
 // ------------------------------------------------------------- arithmetic --
