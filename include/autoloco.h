@@ -21,7 +21,9 @@
  * interface calls it k and uses n for the number of parameters.
  *
  * Device calls run on the HIP stream bound to the context.  Host-only calls
- * (schedule, correction, controller) touch no device.
+ * (schedule, correction, controller) touch no device.  Device calls that do not
+ * return sums to the host only launch kernels on that stream and may be
+ * captured into a HIP graph; calls that return sums wait for them and may not.
  *
  * Conventions for every call:
  *   - Return value: AUTOLOCO_OK or a negative autoloco_status.  No call throws,
