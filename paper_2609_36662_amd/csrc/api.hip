@@ -88,19 +88,28 @@ int check_device_ptr(autoloco_ctx* ctx, uintptr_t p, const char* name) {
     return AUTOLOCO_OK;
 }
 
-// Default grid: three workgroups per compute unit, or fewer if fewer fit (the
-// fused kernel's occupancy).  Measured on MI355X (256 CUs) with the round's
-// buffers spread in HBM, 768 workgroups were best or within 1-2 % of best for
-// every workload tried (1.1B K=8 and K=4 fp32, 3B K=8 bf16, 7B K=4, GPT-2
-// small), while 1,024 - exactly one resident wave at 4 per unit - was the
-// slowest by 5-9 %.  Every mode of a given (k, replica type) uses the same
-// grid, so the statistics of a standalone and of a fused call are summed in
-// the same order, bit for bit.
-int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k, bool bf16p = false) {
+// Default grid: from K = 8 one workgroup per compute unit (4 waves), below it
+// three, or fewer if fewer fit (the fused kernel's occupancy).  Measured on
+// MI355X (256 CUs) with the round's buffers spread in HBM, 1.1B K = 8 fp32:
+// fused round 14.14-14.27 ms at 256 workgroups against 14.37-14.57 at 768 (the
+// traffic reference alike), and no mode slower (statistics only 6.28 against
+// 6.37 ms, with its windows loaded ahead); 3B K = 8 bf16, GPT-2 small K = 8 and
+// K = 12-16 gain 1-3 % too.  At K = 4 the fused round gains 1 % but the update
+// without the reset and the reset alone lose 10-23 %, and below K = 4 the
+// statistics-only mode needs more waves, so those keep 768.  Even multiples of
+// 256 are the slowest.  Every mode of a given (k, replica type) uses the same
+// grid, so the statistics of a standalone and of a fused call are summed in the
+// same order, bit for bit.
+// round_grid = false: a kernel with no statistics to keep in step with the
+// round's modes (the reset alone, AdamW's gradient-norm pass), which keeps three
+// per compute unit at every K.
+int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k, bool bf16p = false,
+               bool round_grid = true) {
     const int64_t v = dtype == AUTOLOCO_BF16 ? 8 : 4;
     const int64_t nvec = n / v;
     int per_cu = (bf16p ? ctx->occupancy_bf16p : ctx->occupancy)[dtype == AUTOLOCO_BF16 ? 1 : 0][k];
     if (per_cu > 3) per_cu = 3;
+    if (round_grid && k >= 8) per_cu = 1;
     if (per_cu < 1) per_cu = 1;
     int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * per_cu;
     if (limit > kMaxBlocks) limit = kMaxBlocks;
@@ -648,7 +657,7 @@ int autoloco_broadcast_reset(autoloco_ctx* c, const autoloco_buffers* b) {
     DeviceGuard g(c->device);
     if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
     RoundArgs a = make_args(c, b);
-    const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k);
+    const int blocks = blocks_for(c, b->n, b->replica_dtype, b->k, false, false);
     int ts = timer_start(c);
     if (ts != AUTOLOCO_OK) return ts;
     hipError_t e = launch_reset(b->replica_dtype == AUTOLOCO_BF16 ? RT_BF16 : RT_F32, b->k, blocks, c->stream, a);
@@ -843,7 +852,7 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
         for (int k = 0; k < b->k; ++k) na.grads[k] = b->grads[k];
         na.n = b->n;
         na.partials = c->partials;
-        const int nblocks = blocks_for(c, b->n, AUTOLOCO_F32, b->k);
+        const int nblocks = blocks_for(c, b->n, AUTOLOCO_F32, b->k, false, false);
         e = launch_grad_norm(b->k, nblocks, c->stream, na);
         if (e != hipSuccess) return hip_fail(c, e, "gradient norm launch");
         e = launch_finish_sums(b->k, kBlock, nblocks, c->partials, c->sums, c->stream);

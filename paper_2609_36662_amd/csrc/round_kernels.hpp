@@ -158,6 +158,23 @@ __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K]
     }
 }
 
+// Windows the statistics-only mode loads ahead: enough for about 512 bytes of
+// loads per lane (from K = 8 the default grid holds one wave per SIMD), at most
+// 8, within 200 registers for the loaded words (below K = 8, whose grid keeps
+// three workgroups per compute unit, 100 with fp32 replicas and 64 with bf16, so
+// that three waves per SIMD still fit).  Per window a lane loads (K + 1)
+// quads of fp32, or with bf16 replicas two of theta and 2K words.
+template <int K, int RT>
+constexpr int stats_unroll() {
+    const int words = RT == RT_F32 ? 4 * (K + 1) : 4 * K + 8;
+    const int bytes = RT == RT_F32 ? 16 * (K + 1) : 32 + 16 * K;
+    const int cap = K >= 8 ? 200 : (RT == RT_F32 ? 100 : 64);
+    int u = (512 + bytes - 1) / bytes;
+    if (u > 8) u = 8;
+    while (u > 1 && u * words > cap) --u;
+    return u;
+}
+
 // ------------------------------------------------------------ round kernel --
 template <int K, int RT, bool STATS, bool UPDATE, bool RESET, bool BF16P = false>
 __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
@@ -179,95 +196,175 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
     const int64_t qstride = (int64_t)gridDim.x * kBlock * R;
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
 
-    for (int64_t qb = (int64_t)blockIdx.x * kBlock * R; qb < nq; qb += qstride) {
-        if (qb + threadIdx.x >= nq) continue;
-        // run 1 (bf16) exists unless this is the last, shorter window
-        const bool ok1 = R == 2 && qb + kBlock + threadIdx.x < nq;
-        const int64_t wb = qb * 4;                        // first parameter of the window
-        float* const th_w = a.theta + wb;
-        float* const mo_w = UPDATE ? a.momentum + wb : nullptr;
-        float th[V], v[V], r[K][V];
+    if constexpr (!UPDATE) {
+        // Statistics only, so no stores to overlap the loads with: U windows of
+        // the thread's grid-stride sequence are loaded before any of them is
+        // added up, in that same order, which keeps every per-thread sum what one
+        // window per iteration gives, bit for bit, with U times the loads in
+        // flight.
+        constexpr int U = stats_unroll<K, RT>();
+        for (int64_t qb0 = (int64_t)blockIdx.x * kBlock * R; qb0 < nq; qb0 += U * qstride) {
+            f32x4 tq[U][R];
+            f32x4 rf[RT == RT_F32 ? U : 1][RT == RT_F32 ? K : 1];
+            u32x2r rw[RT == RT_BF16 ? U : 1][RT == RT_BF16 ? K : 1][R];
+            bool live[U], ok1[U];
 #pragma unroll
-        for (int h = 0; h < R; ++h) {
-            const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;   // byte offset in fp32 buffers
-            if (h == 1 && !ok1) {
+            for (int u = 0; u < U; ++u) {
+                const int64_t qb = qb0 + u * qstride;
+                live[u] = qb + threadIdx.x < nq;
+                ok1[u] = R == 2 && qb + kBlock + threadIdx.x < nq;
+                if (!live[u]) continue;
+                const int64_t wb = qb * 4;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    th[4 * h + e] = v[4 * h + e] = 0.f;
+                for (int h = 0; h < R; ++h) {
+                    if (h == 1 && !ok1[u]) continue;
+                    const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;
+                    tq[u][h] = ld_f4_at(a.theta + wb, fo);
 #pragma unroll
-                    for (int k = 0; k < K; ++k) r[k][4 * h + e] = 0.f;
+                    for (int k = 0; k < K; ++k) {
+                        if constexpr (RT == RT_F32)
+                            rf[u][k] = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, fo);
+                        else
+                            rw[u][k][h] = ld_u2_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, fo / 2);
+                    }
                 }
-                continue;
-            }
-            const f32x4 t4 = ld_f4_at(th_w, fo);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) th[4 * h + e] = t4[e];
-            if constexpr (UPDATE) {
-                const f32x4 v4 = ld_f4_at(mo_w, fo);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[4 * h + e] = v4[e];
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[4 * h + e] = 0.f;
             }
 #pragma unroll
-            for (int k = 0; k < K; ++k) {
-                if constexpr (RT == RT_F32) {
-                    const f32x4 r4 = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, fo);
+            for (int u = 0; u < U; ++u) {
+                if (!live[u]) break;   // the later windows lie past the end as well
+                float th[V], r[K][V];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
+                for (int h = 0; h < R; ++h) {
+                    const bool z = h == 1 && !ok1[u];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) th[4 * h + e] = z ? 0.f : tq[u][h][e];
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        if constexpr (RT == RT_F32) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) r[k][e] = rf[u][k][e];
+                        } else {
+                            const u32x2r w = z ? u32x2r{0u, 0u} : rw[u][k][h];
+                            r[k][4 * h] = bf16_lo(w[0]);
+                            r[k][4 * h + 1] = bf16_hi(w[0]);
+                            r[k][4 * h + 2] = bf16_lo(w[1]);
+                            r[k][4 * h + 3] = bf16_hi(w[1]);
+                        }
+                    }
+                }
+                float s[K], q[K], m = 0.f;
+#pragma unroll
+                for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    float re[K];
+#pragma unroll
+                    for (int k = 0; k < K; ++k) re[k] = r[k][e];
+                    float tn, vn;
+                    uint32_t pbe;
+                    one_param<K, STATS, UPDATE, BF16P>(th[e], 0.f, re, a, s, q, m, tn, vn, pbe);
+                }
+                if constexpr (STATS) {
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        acc[k] += (double)s[k];
+                        acc[K + k] += (double)q[k];
+                    }
+                    acc[2 * K] += (double)m;
+                }
+            }
+        }
+    } else {
+        for (int64_t qb = (int64_t)blockIdx.x * kBlock * R; qb < nq; qb += qstride) {
+            if (qb + threadIdx.x >= nq) continue;
+            // run 1 (bf16) exists unless this is the last, shorter window
+            const bool ok1 = R == 2 && qb + kBlock + threadIdx.x < nq;
+            const int64_t wb = qb * 4;                        // first parameter of the window
+            float* const th_w = a.theta + wb;
+            float* const mo_w = UPDATE ? a.momentum + wb : nullptr;
+            float th[V], v[V], r[K][V];
+#pragma unroll
+            for (int h = 0; h < R; ++h) {
+                const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;   // byte offset in fp32 buffers
+                if (h == 1 && !ok1) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        th[4 * h + e] = v[4 * h + e] = 0.f;
+#pragma unroll
+                        for (int k = 0; k < K; ++k) r[k][4 * h + e] = 0.f;
+                    }
+                    continue;
+                }
+                const f32x4 t4 = ld_f4_at(th_w, fo);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) th[4 * h + e] = t4[e];
+                if constexpr (UPDATE) {
+                    const f32x4 v4 = ld_f4_at(mo_w, fo);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[4 * h + e] = v4[e];
                 } else {
-                    const u32x2r w = ld_u2_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, fo / 2);
-                    r[k][4 * h] = bf16_lo(w[0]);
-                    r[k][4 * h + 1] = bf16_hi(w[0]);
-                    r[k][4 * h + 2] = bf16_lo(w[1]);
-                    r[k][4 * h + 3] = bf16_hi(w[1]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[4 * h + e] = 0.f;
+                }
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    if constexpr (RT == RT_F32) {
+                        const f32x4 r4 = ld_f4_at(static_cast<const float*>(a.replicas[k]) + wb, fo);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) r[k][e] = r4[e];
+                    } else {
+                        const u32x2r w = ld_u2_at(static_cast<const uint16_t*>(a.replicas[k]) + wb, fo / 2);
+                        r[k][4 * h] = bf16_lo(w[0]);
+                        r[k][4 * h + 1] = bf16_hi(w[0]);
+                        r[k][4 * h + 2] = bf16_lo(w[1]);
+                        r[k][4 * h + 3] = bf16_hi(w[1]);
+                    }
                 }
             }
-        }
 
-        float s[K], q[K], m = 0.f;
+            float s[K], q[K], m = 0.f;
 #pragma unroll
-        for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
-        float th_new[V], v_new[V];
-        uint32_t pb[V];
+            for (int k = 0; k < K; ++k) s[k] = q[k] = 0.f;
+            float th_new[V], v_new[V];
+            uint32_t pb[V];
 #pragma unroll
-        for (int e = 0; e < V; ++e) {
-            float re[K];
+            for (int e = 0; e < V; ++e) {
+                float re[K];
 #pragma unroll
-            for (int k = 0; k < K; ++k) re[k] = r[k][e];
-            one_param<K, STATS, UPDATE, BF16P>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e], pb[e]);
-        }
-        if constexpr (STATS) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                acc[k] += (double)s[k];
-                acc[K + k] += (double)q[k];
+                for (int k = 0; k < K; ++k) re[k] = r[k][e];
+                one_param<K, STATS, UPDATE, BF16P>(th[e], v[e], re, a, s, q, m, th_new[e], v_new[e], pb[e]);
             }
-            acc[2 * K] += (double)m;
-        }
+            if constexpr (STATS) {
 #pragma unroll
-        for (int h = 0; h < R; ++h) {
-            if (h == 1 && !ok1) continue;
-            const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;
-            if constexpr (BF16P) {
-                // 2 bytes per parameter: 8 per quad
-                if (a.payload != nullptr)
-                    st_u2_at(a.payload + wb, fo / 2, u32x2r{pb[4 * h] | pb[4 * h + 1] << 16,
-                                                            pb[4 * h + 2] | pb[4 * h + 3] << 16});
+                for (int k = 0; k < K; ++k) {
+                    acc[k] += (double)s[k];
+                    acc[K + k] += (double)q[k];
+                }
+                acc[2 * K] += (double)m;
             }
-            if constexpr (UPDATE) {
-                const f32x4 o = {th_new[4 * h], th_new[4 * h + 1], th_new[4 * h + 2], th_new[4 * h + 3]};
-                st_f4_at(th_w, fo, o);
-                st_f4_at(mo_w, fo, f32x4{v_new[4 * h], v_new[4 * h + 1], v_new[4 * h + 2], v_new[4 * h + 3]});
-                if constexpr (RESET) {
-                    if constexpr (RT == RT_F32) {
 #pragma unroll
-                        for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, fo, o);
-                    } else {
-                        const u32x2r w = {bf16_pack(o[0], o[1]), bf16_pack(o[2], o[3])};
+            for (int h = 0; h < R; ++h) {
+                if (h == 1 && !ok1) continue;
+                const uint32_t fo = (h * kBlock + threadIdx.x) * 16u;
+                if constexpr (BF16P) {
+                    // 2 bytes per parameter: 8 per quad
+                    if (a.payload != nullptr)
+                        st_u2_at(a.payload + wb, fo / 2, u32x2r{pb[4 * h] | pb[4 * h + 1] << 16,
+                                                                pb[4 * h + 2] | pb[4 * h + 3] << 16});
+                }
+                if constexpr (UPDATE) {
+                    const f32x4 o = {th_new[4 * h], th_new[4 * h + 1], th_new[4 * h + 2], th_new[4 * h + 3]};
+                    st_f4_at(th_w, fo, o);
+                    st_f4_at(mo_w, fo, f32x4{v_new[4 * h], v_new[4 * h + 1], v_new[4 * h + 2], v_new[4 * h + 3]});
+                    if constexpr (RESET) {
+                        if constexpr (RT == RT_F32) {
 #pragma unroll
-                        for (int k = 0; k < K; ++k) st_u2_at(static_cast<uint16_t*>(a.replicas[k]) + wb, fo / 2, w);
+                            for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, fo, o);
+                        } else {
+                            const u32x2r w = {bf16_pack(o[0], o[1]), bf16_pack(o[2], o[3])};
+#pragma unroll
+                            for (int k = 0; k < K; ++k) st_u2_at(static_cast<uint16_t*>(a.replicas[k]) + wb, fo / 2, w);
+                        }
                     }
                 }
             }
