@@ -12,6 +12,7 @@ import pytest
 import paper_2609_36662_amd as al
 from oracle import controller as oc
 from oracle import correction as ocorr
+from tests import controller_pins
 from tests.controller_driver import Event, drive
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -171,6 +172,15 @@ def test_controller_matches_oracle_decision_by_decision(name):
     if ties:
         warnings.warn(f"near-tie z values in scenario {name}: {ties}")
     _replay(cfg, obs, decs)
+
+
+@pytest.mark.parametrize("name", [n for n, _ in controller_pins.SCENARIOS])
+def test_controller_matches_oracle_on_hand_derived_pins(name):
+    # the hand-derived scenarios of the reference EMA, the MAD scale and the
+    # H_min fallback, replayed observation by observation
+    script, checks = dict(controller_pins.SCENARIOS)[name]()
+    assert controller_pins.failures(checks) == []
+    _replay(script.cfg, script.observations, script.decisions)
 
 
 def test_controller_reproduces_c4_trajectory():
