@@ -354,7 +354,7 @@ def bench_inner(args) -> int:
 
 SHARE_METRIC = "per-GPU share of a one-replica-per-GPU round (BF16 payloads) params/s, 1.1B params K=8 GPUs"
 SHARE_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "shard_inst.hip", "round_kernels.hpp",
-                                                  "reduce.hpp")]
+                                                  "reduce.hpp", "reset_kernels.hpp")]
 
 
 def bench_share(args) -> int:
@@ -426,6 +426,27 @@ def bench_share(args) -> int:
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step wall; payload {tp:.3f} ms "
         f"({b_payload / tp / 1e6:.0f} GB/s), shard step {tsh:.3f} ms ({b_shard / tsh / 1e6:.0f} GB/s), "
         f"reset {tr:.3f} ms ({b_reset / tr / 1e6:.0f} GB/s)")
+    # each kernel's traffic reference: the probe of its own loads and stores
+    # (same shape and grid, no arithmetic)
+    num_cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    R, W, RW = al.PROBE_READ, al.PROBE_WRITE, al.PROBE_READ | al.PROBE_WRITE
+    refs = {
+        "payload": ([(theta, R), (rep, R), (payload, W)], al.PROBE_RUN2, args.grid or 2 * num_cus),
+        "shard_step": ([(theta[:ns], RW), (v_shard, RW)] + [(r, R) for r in recv] + [(mean, W)], al.PROBE_RUN2,
+                       args.grid or 2 * num_cus),
+        # the reset alone runs three workgroups per compute unit
+        "reset": ([(theta, R), (rep, W)], al.PROBE_RUN1 if rdt == "f32" else al.PROBE_RUN2,
+                  args.grid or 3 * num_cus),
+    }
+    ref_ms = {}
+    for name, (streams, shape, blocks) in refs.items():
+        ms = []
+        for rep_i in range(args.warmup + args.steps):
+            al.autoloco_traffic_probe(ctx, streams, shape, blocks)
+            if rep_i >= args.warmup:
+                ms.append(al.autoloco_last_kernel_ms(ctx))
+        ref_ms[name] = statistics.median(ms)
+    log("traffic references: " + ", ".join(f"{k_} {v:.3f} ms" for k_, v in ref_ms.items()))
     achieved = b_payload / (tp * 1e-3) / 1e9
     ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
     traffic = committed_traffic(f"share_{rdt}_k{k}_{args.workload}", SHARE_SOURCES)
@@ -455,6 +476,9 @@ def bench_share(args) -> int:
         },
         "copy_ceiling_gbs": ceiling,
         "kernel_ms": {"payload": tp, "shard_step": tsh, "reset": tr},
+        "traffic_reference_ms": ref_ms,
+        "ratio_to_reference": {"payload": tp / ref_ms["payload"], "shard_step": tsh / ref_ms["shard_step"],
+                               "reset": tr / ref_ms["reset"]},
         "kernel_gbs": {"payload": b_payload / tp / 1e6, "shard_step": b_shard / tsh / 1e6,
                        "reset": b_reset / tr / 1e6},
         "cpu_baseline": None,
@@ -462,6 +486,226 @@ def bench_share(args) -> int:
     }
     print(json.dumps(out), flush=True)
     del ts, theta, rep, inp, recv, payload, v_shard, mean
+    ctx.close()
+    return 0
+
+
+RESET_METRIC = "standalone replica reset params/s and achieved HBM GB/s (% of peak), 1.1B params K=8"
+RESET_SOURCES = [os.path.join(CSRC, f) for f in ("reset_kernels.hpp", "round_kernels.hpp")]
+
+
+def bench_reset(args) -> int:
+    """The standalone reset (theta_k <- theta for every replica; Alg. "AutoLoCo
+    outer interval") at the library's default grid, beside the probe of its own
+    loads and stores (theta read, K replicas written) at the same grid."""
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift, shapes
+
+    shape_name, k, rdt = WORKLOADS[args.workload][0], WORKLOADS[args.workload][1], WORKLOADS[args.workload][2]
+    if args.k:
+        k = args.k
+    n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
+    s_r = 4 if rdt == "f32" else 2
+    nbytes = n * (4 + k * s_r)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ctx = al.autoloco_create(0)
+    ts, spread = al.spread_tensors(ctx, n, [torch.float32] + [tdtype] * k)
+    theta, reps = ts[0], ts[1:]
+    drift._normal_into(theta, 0.02, 42, drift.ROLE_THETA, 0)
+    torch.cuda.synchronize()
+    num_cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    if args.grid:
+        al.autoloco_set_grid_limit(ctx, args.grid)
+    al.autoloco_set_timing(ctx, True)
+    log(f"reset {args.workload}: n={n:,} K={k} {rdt} replicas, {nbytes / 1e9:.2f} GB per reset "
+        f"({'spread' if spread else 'plain'} buffers)")
+
+    def median_ms(call):
+        ms = []
+        for i in range(args.warmup + args.steps):
+            call()
+            if i >= args.warmup:
+                ms.append(al.autoloco_last_kernel_ms(ctx))
+        return statistics.median(ms)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        al.autoloco_broadcast_reset(ctx, theta, reps)
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) / args.steps * 1e3
+    ms = median_ms(lambda: al.autoloco_broadcast_reset(ctx, theta, reps))
+    # the reset's own pattern at its grid (three workgroups per compute unit)
+    blocks = args.grid or 3 * num_cus
+    shape = al.PROBE_RUN1 if rdt == "f32" else al.PROBE_RUN2
+    ref_ms = median_ms(lambda: al.autoloco_traffic_probe(ctx, [(theta, al.PROBE_READ)] +
+                                                         [(r, al.PROBE_WRITE) for r in reps], shape, blocks))
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    log(f"reset {ms:.3f} ms ({achieved:.0f} GB/s, {100 * achieved / PEAK_HBM_GBS:.1f} %), its pattern {ref_ms:.3f} ms: "
+        f"{ms / ref_ms:.4f} x")
+    ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
+    out = {
+        "metric": metric_name(RESET_METRIC, args, k), "value": n / (ms_per_step * 1e-3), "unit": "params/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if rdt == "f32" else "f32 (bf16 replicas)", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: theta ({n:,} fp32) into K={k} {rdt} replicas",
+                   "n_params": n, "k": k, "bytes": nbytes, "alloc": alloc_label("spread", spread)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "reset_kernel"},
+        "kernel_ms_median": ms, "traffic_reference_ms_median": ref_ms, "ratio_to_reference": ms / ref_ms,
+        "copy_ceiling_gbs": ceiling, "cpu_baseline": None,
+        "kernel_source_sha256_16": kernel_source_hash(RESET_SOURCES),
+    }
+    print(json.dumps(out), flush=True)
+    del ts, theta, reps
+    ctx.close()
+    return 0
+
+
+PROBE_METRIC = ("streaming-pattern probes: HBM GB/s (% of peak) of access patterns on the buffers of the 1.1B "
+                "params K=8 round, and the standalone reset against its pattern")
+
+
+def bench_probe(args) -> int:
+    """What the device sustains for streaming access patterns on the round's own
+    buffers (theta, v and 8 fp32 replicas of the 1.1B model, 4.4 GB each): the
+    round's ten streams in place, the same streams read only or written only,
+    fewer streams, out of place, LDS-staged tiles; then the fused round and its
+    traffic reference, and the standalone reset at K = 8 and K = 1 beside the
+    probe of its own pattern (one stream read, K written), over grids."""
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift, shapes
+
+    n = shapes.SHAPES["llama-1.1b"]().n_params
+    k = 8
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ctx = al.autoloco_create(0)
+    spread = False
+    if args.alloc == "spread":
+        ts, spread = al.spread_tensors(ctx, n, [torch.float32] * (k + 2))
+    else:
+        ts = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(k + 2)]
+    inp = drift.RoundInputs(ts[0], ts[1], ts[2:])
+    drift.fill_theta_momentum(inp, seed=42, recipe=drift.MIXED)
+    drift.fill_replicas(inp, seed=42, recipe=drift.MIXED)
+    torch.cuda.synchronize()
+    num_cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    al.autoloco_set_timing(ctx, True)
+    R, W, RW = al.PROBE_READ, al.PROBE_WRITE, al.PROBE_READ | al.PROBE_WRITE
+    log(f"probe buffers: {k + 2} x {n * 4 / 1e9:.2f} GB ({'spread' if spread else 'plain'}); {num_cus} CUs")
+
+    def timed(call):
+        times = []
+        moved = 0.0
+        for rep in range(args.warmup + args.steps):
+            moved = call()
+            ms = al.autoloco_last_kernel_ms(ctx)
+            if rep >= args.warmup:
+                times.append(ms)
+        return moved, statistics.median(times), min(times)
+
+    def probe(name, shape, spec, blocks=0):
+        streams = [(ts[i], acc) for i, acc in spec]
+        moved, med, best = timed(lambda: al.autoloco_traffic_probe(ctx, streams, shape, blocks))
+        row = {"pattern": name, "shape": ["run1", "run2", "serial", "tile"][shape],
+               "blocks": blocks or num_cus, "bytes": moved, "ms_median": med, "ms_min": best,
+               "gbs": moved / med / 1e6, "frac_of_peak": moved / med / 1e6 / PEAK_HBM_GBS}
+        log(f"  {name:52s} {row['shape']:6s} {row['blocks']:5d} wg  {med:8.3f} ms  {row['gbs']:7.0f} GB/s "
+            f"({100 * row['frac_of_peak']:.1f} %)")
+        return row
+
+    # every pattern over grids from one workgroup per compute unit to eight:
+    # patterns with few streams need more waves to keep enough bytes in flight
+    grids = [num_cus * m for m in (1, 2, 3, 4, 8)]
+    ten = list(range(k + 2))
+    patterns = [
+        ("10 streams in place (the round's pattern)", al.PROBE_RUN1, [(i, RW) for i in ten]),
+        ("10 streams read", al.PROBE_RUN1, [(i, R) for i in ten]),
+        ("10 streams written", al.PROBE_RUN1, [(i, W) for i in ten]),
+        ("1 stream read", al.PROBE_RUN1, [(0, R)]),
+        ("2 streams read", al.PROBE_RUN1, [(i, R) for i in range(2)]),
+        ("4 streams read", al.PROBE_RUN1, [(i, R) for i in range(4)]),
+        ("1 stream written", al.PROBE_RUN1, [(0, W)]),
+        ("1 stream in place", al.PROBE_RUN1, [(0, RW)]),
+        ("2 streams in place", al.PROBE_RUN1, [(i, RW) for i in range(2)]),
+        ("4 streams in place", al.PROBE_RUN1, [(i, RW) for i in range(4)]),
+        ("6 streams in place", al.PROBE_RUN1, [(i, RW) for i in range(6)]),
+        ("5 streams read, 5 others written", al.PROBE_RUN1, [(i, R) for i in range(5)] + [(i, W) for i in range(5, 10)]),
+        ("10 streams in place, two runs per lane", al.PROBE_RUN2, [(i, RW) for i in ten]),
+    ]
+    rows = []
+    for name, shape, spec in patterns:
+        sweep = [probe(name, shape, spec, g) for g in grids]
+        best = max(sweep, key=lambda r: r["gbs"])
+        rows.append({**best, "at_one_per_cu_gbs": sweep[0]["gbs"], "grids": {r["blocks"]: r["gbs"] for r in sweep}})
+    # LDS tiles hold 160 KB of one workgroup: one per compute unit
+    for name, shape, spec in (
+            ("10 streams in place, LDS tiles stream by stream", al.PROBE_SERIAL, [(i, RW) for i in ten]),
+            ("10 streams in place, LDS tiles all streams at once", al.PROBE_TILE, [(i, RW) for i in ten]),
+            ("10 streams read, LDS tiles stream by stream", al.PROBE_SERIAL, [(i, R) for i in ten]),
+            ("10 streams read, LDS tiles all streams at once", al.PROBE_TILE, [(i, R) for i in ten]),
+            ("10 streams written, LDS tiles", al.PROBE_TILE, [(i, W) for i in ten])):
+        rows.append(probe(name, shape, spec, num_cus))
+
+    # the fused round and its traffic reference on the same buffers
+    coeffs = al.autoloco_outer_correction(al.make_outer_cfg(), al.autoloco_lr_mass(al.make_schedule(), 20_000, 750),
+                                          al.autoloco_lr_mass(al.make_schedule(), 20_000, 500))
+    flags = al.FUSE_STATS | al.FUSE_RESET
+    b_round = n * (2 * k * 4 + 16)
+
+    def round_call():
+        al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, coeffs, flags, 1e-12)
+        return b_round
+
+    def ref_call():
+        al.autoloco_traffic_reference(ctx, inp.theta, inp.momentum, inp.replicas)
+        return b_round
+
+    kernels = []
+    for name, call in (("fused round (round_kernel)", round_call), ("traffic reference (traffic_kernel)", ref_call)):
+        moved, med, best = timed(call)
+        kernels.append({"kernel": name, "bytes": moved, "ms_median": med, "gbs": moved / med / 1e6})
+        log(f"  {name:48s} {med:8.3f} ms  {moved / med / 1e6:7.0f} GB/s")
+
+    # standalone reset (theta read, K replicas written) against the probe of that pattern
+    resets = []
+    for kk in (8, 1):
+        b_reset = n * (4 + 4 * kk)
+        for blocks in (256, 512, 768, 1024):
+            al.autoloco_set_grid_limit(ctx, blocks)
+            _, med, _ = timed(lambda: (al.autoloco_broadcast_reset(ctx, inp.theta, inp.replicas[:kk]), b_reset)[1])
+            al.autoloco_set_grid_limit(ctx, 0)
+            ref = probe(f"reset pattern K={kk}: 1 stream read, {kk} written", al.PROBE_RUN1,
+                        [(0, R)] + [(2 + j, W) for j in range(kk)], blocks)
+            # the reset wrote theta into the replicas; the probe writes them the same words
+            resets.append({"k": kk, "blocks": blocks, "bytes": b_reset, "reset_ms_median": med,
+                           "reset_gbs": b_reset / med / 1e6, "reference_ms_median": ref["ms_median"],
+                           "ratio_to_reference": med / ref["ms_median"]})
+            log(f"  reset K={kk} at {blocks:5d} wg: {med:.3f} ms ({b_reset / med / 1e6:.0f} GB/s), "
+                f"{med / ref['ms_median']:.3f} x its pattern")
+        _, med, _ = timed(lambda: (al.autoloco_broadcast_reset(ctx, inp.theta, inp.replicas[:kk]), b_reset)[1])
+        resets.append({"k": kk, "blocks": "default", "bytes": b_reset, "reset_ms_median": med,
+                       "reset_gbs": b_reset / med / 1e6})
+        log(f"  reset K={kk} at the default grid: {med:.3f} ms ({b_reset / med / 1e6:.0f} GB/s)")
+
+    best = max(r["gbs"] for r in rows if r["pattern"].startswith("10 streams in place"))
+    log("best of each pattern: " + "; ".join(f"{r['pattern']} {r['gbs']:.0f} GB/s at {r['blocks']}" for r in rows))
+    out = {
+        "metric": PROBE_METRIC, "value": best, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "higher_is_better": True, "data": "synthetic",
+        "config": {"workload": f"llama-1.1b buffers: {k + 2} x {n:,} fp32 elements",
+                   "alloc": alloc_label(args.alloc, spread), "cus": num_cus},
+        "probes": rows, "kernels": kernels, "reset": resets,
+        "kernel_source_sha256_16": kernel_source_hash(KERNEL_SOURCES + [os.path.join(CSRC, "probe_kernels.hpp")]),
+    }
+    print(json.dumps(out), flush=True)
+    del ts, inp
     ctx.close()
     return 0
 
@@ -609,11 +853,13 @@ def main() -> int:
     ap.add_argument("--no-ceiling", action="store_true")
     ap.add_argument("--perturbed", type=int, default=20,
                     help="extra rounds, each on freshly drawn replicas (drawn outside the timing)")
-    ap.add_argument("--step", choices=("round", "inner", "share", "closed-loop"), default="round",
+    ap.add_argument("--step", choices=("round", "inner", "share", "closed-loop", "probe", "reset"), default="round",
                     help="round: the synchronisation round; inner: one AdamW step of every worker; share: one "
                          "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives); "
                          "closed-loop: consecutive rounds with the interval controller choosing each one's "
-                         "coefficients from the previous round's statistics (use --workload llama-7b)")
+                         "coefficients from the previous round's statistics (use --workload llama-7b); probe: "
+                         "streaming-pattern probes on the round's buffers (the device's ceiling for each pattern); "
+                         "reset: the standalone replica reset beside the probe of its own loads and stores")
     ap.add_argument("--copy", action="store_true", help="inner: also write each worker's BF16 compute copy")
     args = ap.parse_args()
 
@@ -626,6 +872,10 @@ def main() -> int:
         return bench_inner(args)
     if args.step == "share":
         return bench_share(args)
+    if args.step == "probe":
+        return bench_probe(args)
+    if args.step == "reset":
+        return bench_reset(args)
     if args.step == "closed-loop":
         return bench_closed_loop(args)
 

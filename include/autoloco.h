@@ -175,7 +175,8 @@ typedef struct {
 
 /* Statistics of one round (eq. adaptive-h-core-diagnostics; App. C.1):
  * reads theta and the k replicas once, writes nothing but *out.  Blocks until
- * the sums are on the host.  eps >= 0 is the constant in C.  Stats of the same
+ * the sums are on the host.  eps > 0 (finite) is the constant in C, so that
+ * D = 0 (every replica equal to theta) gives C = 0.  Stats of the same
  * buffers are bit-identical from run to run (fixed reduction order).
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
 int autoloco_round_stats(autoloco_ctx* ctx, const autoloco_buffers* bufs, double eps,
@@ -249,6 +250,57 @@ int autoloco_broadcast_reset(autoloco_ctx* ctx, const autoloco_buffers* bufs);
  * Asynchronous on the stream.  Buffers as autoloco_outer_step.
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
 int autoloco_traffic_reference(autoloco_ctx* ctx, const autoloco_buffers* bufs);
+
+/* Streaming-pattern probe (measurement only, no operation of the paper): moves
+ * the bytes of `count` streams with no arithmetic, so its device time is what
+ * the device sustains for that access pattern on those buffers — for instance
+ * the round's ten streams in place, the same buffers read only or written
+ * only, or the loads and stores of the reset and of the per-GPU kernels.
+ *   streams[s].ptr: device buffer of n elements of streams[s].elem_bytes (4 or
+ *     2); 16-byte aligned; no two overlap.
+ *   streams[s].access: AUTOLOCO_PROBE_READ, AUTOLOCO_PROBE_WRITE or both (both:
+ *     4-byte streams only; each word is written back unchanged).  Written-only
+ *     streams receive the words of stream 0 (2-byte streams: the upper halves
+ *     of its words) when stream 0 is read, else the index of each run of 4, so
+ *     they lose their contents.
+ *   The streams come in this order of classes: 4-byte read and written, 4-byte
+ *     read, 2-byte read, 2-byte written, 4-byte written; only the class counts
+ *     the library instantiates are accepted (E_INVALID otherwise): with
+ *     AUTOLOCO_PROBE_RUN1 (the fp32 round's window loop, one run of 4 elements
+ *     per lane per window) 1, 2, 4, 6 or 10 streams in place, 1, 2, 4 or 10
+ *     read, 1 or 10 written, 5 read and 5 written, 1 read and 1, 4, 8 or 16
+ *     written; with AUTOLOCO_PROBE_RUN2 (two runs per lane, 256 runs apart: the
+ *     bf16 round's and the per-GPU kernels' shape) 10 in place or read, one 4-byte read
+ *     and 1, 4, 8 or 16 2-byte written, two 4-byte read (or one 4-byte and one
+ *     2-byte) and one 2-byte written, two 4-byte in place with 1, 2, 4, 8 or 16
+ *     2-byte read and one 2-byte written (or, for 4 and 8, none); with
+ *     AUTOLOCO_PROBE_SERIAL (every workgroup stages 16 KB of each read stream
+ *     in LDS with direct loads, stream after stream, at most two streams'
+ *     loads in flight, then stores stream by stream) and AUTOLOCO_PROBE_TILE
+ *     (the same tiles with all streams' loads in flight at once) 10 streams in
+ *     place, read, or written.  Run shapes skip the last n mod 4 elements, tile
+ *     shapes the elements past the last whole tile of 4,096.
+ *   blocks: workgroups (256 threads), 0 = one per compute unit.
+ *   *bytes (may be NULL) receives the bytes moved (reads plus writes).
+ * Asynchronous on the stream; timed like the other calls.
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+#define AUTOLOCO_PROBE_READ 1
+#define AUTOLOCO_PROBE_WRITE 2
+#define AUTOLOCO_PROBE_RUN1 0
+#define AUTOLOCO_PROBE_RUN2 1
+#define AUTOLOCO_PROBE_SERIAL 2
+#define AUTOLOCO_PROBE_TILE 3
+typedef struct {
+    void* ptr;
+    int32_t elem_bytes;
+    int32_t access;
+} autoloco_probe_stream;
+int autoloco_traffic_probe(autoloco_ctx* ctx, int64_t n, const autoloco_probe_stream* streams, int32_t count,
+                           int32_t shape, int32_t blocks, double* bytes);
+
+/* Hash of the source files this library was built from (static storage).  A
+ * binding compares it with the sources beside it to refuse a stale build. */
+const char* autoloco_build_id(void);
 
 /* ------------------------------------------------------------------------ */
 /* One GPU's share of a round with one worker replica per GPU                */
@@ -396,7 +448,7 @@ int autoloco_outer_correction(const autoloco_outer_cfg* cfg, double lambda_sel,
 typedef struct {
     int64_t h_base, h_min, h_max, q_h, budget_steps;
     double beta_tok;      /* token-density EMA coefficient (0.9) */
-    double eps;           /* numerical constant of the residuals and the mapper */
+    double eps;           /* numerical constant of the residuals and the mapper, > 0 */
     double thr_cand, thr_mod, thr_sev; /* z_max class limits 1.5 / 2.5 / 4.0 */
     double cand_exposure; /* candidate LR-exposure multiplier 1.15 */
     double retire_frac;   /* rejected-bound retirement fraction 0.90 */

@@ -99,6 +99,10 @@ class ShardBuffers(C.Structure):
                 ("payloads", C.c_void_p * MAX_K)]
 
 
+class ProbeStream(C.Structure):
+    _fields_ = [("ptr", C.c_void_p), ("elem_bytes", C.c_int32), ("access", C.c_int32)]
+
+
 class AdamWBuffers(C.Structure):
     _fields_ = [("n", C.c_int64), ("k", C.c_int32), ("params", C.c_void_p * MAX_K),
                 ("exp_avg", C.c_void_p * MAX_K), ("exp_avg_sq", C.c_void_p * MAX_K),
@@ -142,6 +146,9 @@ SYMBOLS = [
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_traffic_reference", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
+    ("autoloco_traffic_probe", C.c_int, [C.c_void_p, C.c_int64, C.POINTER(ProbeStream), C.c_int32, C.c_int32,
+                                         C.c_int32, C.POINTER(C.c_double)]),
+    ("autoloco_build_id", C.c_char_p, []),
     ("autoloco_rank_payload", C.c_int, [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
                                         C.POINTER(C.c_double)]),
     ("autoloco_shard_step", C.c_int, [C.c_void_p, C.POINTER(ShardBuffers), C.POINTER(OuterCoeffs), C.c_void_p,
@@ -164,13 +171,22 @@ SYMBOLS = [
 ]
 
 
+def check_build_id(handle, expected: str) -> None:
+    """Refuses a library built from sources other than the ones beside it."""
+    got = handle.autoloco_build_id().decode()
+    if got != expected:
+        raise RuntimeError(f"{LIB_PATH} was built from other sources (build id {got}, sources {expected}); "
+                           "rebuild it: python -m paper_2609_36662_amd.build")
+
+
 def lib():
-    """The loaded library; builds it first if nothing is built yet."""
+    """The loaded library; builds it first if nothing is built yet, and refuses
+    one built from other sources than those in this tree."""
     global _lib
     with _lock:
         if _lib is None:
+            from . import build as _build
             if not os.path.exists(LIB_PATH):
-                from . import build as _build
                 _build.build()
             if not os.path.exists(LIB_PATH):
                 raise RuntimeError(f"{LIB_PATH} is missing and could not be built")
@@ -179,6 +195,7 @@ def lib():
                 fn = getattr(handle, name)
                 fn.restype = res
                 fn.argtypes = args
+            check_build_id(handle, _build.source_hash())
             _lib = handle
         return _lib
 
@@ -508,6 +525,36 @@ def autoloco_traffic_reference(ctx: Context, theta, momentum, replicas, n=None) 
 
 
 # -------------------------------------------------------- host scalars --
+PROBE_READ, PROBE_WRITE = 1, 2
+PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE = 0, 1, 2, 3
+
+
+def autoloco_traffic_probe(ctx: Context, streams: Sequence, shape: int = PROBE_RUN1, blocks: int = 0,
+                           n: Optional[int] = None) -> float:
+    """Streaming-pattern probe: streams is a sequence of (tensor, access) with
+    access PROBE_READ, PROBE_WRITE or both; returns the bytes moved."""
+    import torch
+    if not streams:
+        raise ValueError("no streams")
+    if n is None:
+        n = streams[0][0].numel()
+    arr = (ProbeStream * len(streams))()
+    for i, (t, access) in enumerate(streams):
+        if not t.is_cuda or not t.is_contiguous() or t.numel() < n:
+            raise ValueError(f"stream {i}: need a contiguous device tensor of at least {n} elements")
+        if t.dtype not in (torch.float32, torch.bfloat16, torch.int32, torch.int16):
+            raise TypeError(f"stream {i}: 4- or 2-byte elements only")
+        arr[i] = ProbeStream(t.data_ptr(), t.element_size(), int(access))
+    moved = C.c_double()
+    _check(lib().autoloco_traffic_probe(ctx.handle, int(n), arr, len(streams), int(shape), int(blocks),
+                                        C.byref(moved)), "autoloco_traffic_probe", ctx)
+    return moved.value
+
+
+def autoloco_build_id() -> str:
+    return lib().autoloco_build_id().decode()
+
+
 def make_adamw_coeffs(lr: float, step: int, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1,
                       max_grad_norm=1.0) -> AdamWCoeffs:
     """Settings of one inner step (defaults: the C4 recipe)."""

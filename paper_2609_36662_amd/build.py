@@ -7,6 +7,7 @@ shared library next to this file.
 """
 from __future__ import annotations
 
+import hashlib
 import os
 import shutil
 import subprocess
@@ -28,6 +29,29 @@ HIP_FLAGS = [
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-ffp-contract=off", "-fno-fast-math", f"-I{INCLUDE}"]
+
+
+def source_files(root: str = ROOT):
+    """The files the library is built from: the C++/HIP sources, the header and
+    this build script (its flags shape the code)."""
+    csrc = os.path.join(root, "paper_2609_36662_amd", "csrc")
+    inc = os.path.join(root, "include")
+    files = [os.path.join(csrc, f) for f in sorted(os.listdir(csrc)) if f.endswith((".hip", ".hpp", ".cpp"))]
+    files += [os.path.join(inc, f) for f in sorted(os.listdir(inc)) if f.endswith(".h")]
+    files.append(os.path.join(root, "paper_2609_36662_amd", "build.py"))
+    return files
+
+
+def source_hash(root: str = ROOT) -> str:
+    """SHA-256 (first 16 hex digits) over the names and contents of source_files()."""
+    h = hashlib.sha256()
+    for path in source_files(root):
+        h.update(os.path.relpath(path, root).replace(os.sep, "/").encode())
+        h.update(b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
 
 
 def _hipcc() -> str:
@@ -63,7 +87,9 @@ def jobs():
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "adamw_inst.hip"), "-o", os.path.join(BUILD, "adamw.o")])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "shard_inst.hip"), "-o", os.path.join(BUILD, "shard.o")])
     cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "reduce_inst.hip"), "-o", os.path.join(BUILD, "reduce.o")])
-    cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "api.hip"), "-o", os.path.join(BUILD, "api.o")])
+    cmds.append([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "probe_inst.hip"), "-o", os.path.join(BUILD, "probe.o")])
+    cmds.append([hipcc, *HIP_FLAGS, f'-DAUTOLOCO_BUILD_ID="{source_hash()}"', "-c", os.path.join(CSRC, "api.hip"),
+                 "-o", os.path.join(BUILD, "api.o")])
     for src in ("scalar.cpp", "controller.cpp"):
         cmds.append(["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, src),
                      "-o", os.path.join(BUILD, src.replace(".cpp", ".o"))])

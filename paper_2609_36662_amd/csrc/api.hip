@@ -14,8 +14,15 @@
 #include "adamw_kernels.hpp"
 #include "shard_kernels.hpp"
 #include "int8_kernels.hpp"
+#include "probe_kernels.hpp"
+#include "reset_kernels.hpp"
 #include "round_kernels.hpp"
 #include "traffic_kernels.hpp"
+
+// Hash of the sources the library was built from (set by the build).
+#ifndef AUTOLOCO_BUILD_ID
+#define AUTOLOCO_BUILD_ID "unknown"
+#endif
 
 using namespace autoloco;
 
@@ -392,7 +399,8 @@ int validate_step(autoloco_ctx* c, const autoloco_buffers* b, const autoloco_out
     *stats = (flags & AUTOLOCO_FUSE_STATS) != 0;
     *reset = (flags & AUTOLOCO_FUSE_RESET) != 0;
     if (*stats && out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "FUSE_STATS needs a stats output");
-    if (*stats && !(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    // C = K ||mean||^2 / (D + eps) with eps > 0 (eq. adaptive-h-core-diagnostics), so D = 0 gives C = 0
+    if (*stats && !(eps > 0.0 && std::isfinite(eps))) return fail(c, AUTOLOCO_E_INVALID, "eps must be finite and > 0");
     return check_coeffs(c, co);
 }
 
@@ -508,7 +516,7 @@ int autoloco_round_stats(autoloco_ctx* c, const autoloco_buffers* b, double eps,
     int st = validate(c, b, false);
     if (st != AUTOLOCO_OK) return st;
     if (out == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null stats output");
-    if (!(eps >= 0.0)) return fail(c, AUTOLOCO_E_INVALID, "eps must be >= 0");
+    if (!(eps > 0.0 && std::isfinite(eps))) return fail(c, AUTOLOCO_E_INVALID, "eps must be finite and > 0");
     if (b->n == 0) {
         zero_stats(b->k, eps, out);
         return AUTOLOCO_OK;
@@ -683,6 +691,81 @@ int autoloco_traffic_reference(autoloco_ctx* c, const autoloco_buffers* b) {
     c->err.clear();
     return AUTOLOCO_OK;
 }
+
+int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stream* streams, int32_t count,
+                           int32_t shape, int32_t blocks, double* bytes) {
+    if (c == nullptr) return AUTOLOCO_E_INVALID;
+    if (streams == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null streams");
+    if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_TILE)
+        return fail(c, AUTOLOCO_E_INVALID, "unknown probe shape");
+    if (count < 1 || count > kProbeMaxStreams) return fail(c, AUTOLOCO_E_INVALID, "stream count outside 1..18");
+    if (blocks < 0 || blocks > kMaxBlocks) return fail(c, AUTOLOCO_E_INVALID, "blocks outside 0..16384");
+    // classes in order: 4-byte in place, 4-byte read, 2-byte read, 2-byte written, 4-byte written
+    int cls_count[5] = {0, 0, 0, 0, 0};
+    int last = 0;
+    std::vector<Range> r;
+    for (int s = 0; s < count; ++s) {
+        const autoloco_probe_stream& x = streams[s];
+        const bool rd = x.access == AUTOLOCO_PROBE_READ || x.access == (AUTOLOCO_PROBE_READ | AUTOLOCO_PROBE_WRITE);
+        const bool wr = x.access == AUTOLOCO_PROBE_WRITE || x.access == (AUTOLOCO_PROBE_READ | AUTOLOCO_PROBE_WRITE);
+        if (!rd && !wr) return fail(c, AUTOLOCO_E_INVALID, "access must be read, write or both");
+        int cls;
+        if (x.elem_bytes == 4)
+            cls = rd && wr ? 0 : rd ? 1 : 4;
+        else if (x.elem_bytes == 2 && !(rd && wr))
+            cls = rd ? 2 : 3;
+        else
+            return fail(c, AUTOLOCO_E_INVALID, "streams are 4-byte, or 2-byte read only or written only");
+        if (cls < last)
+            return fail(c, AUTOLOCO_E_INVALID, "streams must come in class order: 4-byte in place, 4-byte read, "
+                                               "2-byte read, 2-byte written, 4-byte written");
+        last = cls;
+        ++cls_count[cls];
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(x.ptr);
+        r.push_back({lo, lo + static_cast<uintptr_t>(n) * static_cast<uintptr_t>(x.elem_bytes), "probe stream"});
+    }
+    ProbePattern p;
+    p.shape = shape == AUTOLOCO_PROBE_SERIAL ? PROBE_SERIAL : shape == AUTOLOCO_PROBE_TILE ? PROBE_TILE : PROBE_RUN;
+    p.r = shape == AUTOLOCO_PROBE_RUN2 ? 2 : 1;
+    p.a = cls_count[0];
+    p.b = cls_count[1];
+    p.c = cls_count[2];
+    p.d = cls_count[3];
+    p.e = cls_count[4];
+    if (!probe_available(p)) return fail(c, AUTOLOCO_E_INVALID, "no probe instance for this pattern and shape");
+    if (n == 0) {
+        if (bytes) *bytes = 0.0;
+        return AUTOLOCO_OK;
+    }
+    const int st = check_ranges(c, r);
+    if (st != AUTOLOCO_OK) return st;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    ProbeArgs a;
+    std::memset(&a, 0, sizeof(a));
+    for (int s = 0; s < count; ++s) a.ptr[s] = streams[s].ptr;
+    a.n = n;
+    a.sentinel = 0x9E3779B9u;
+    a.sink = reinterpret_cast<uint32_t*>(c->partials);
+    // elements the shape moves per stream: whole runs of 4, or whole tiles
+    const int64_t tile = 4 * kProbeTileQuads * kBlock;
+    const int64_t moved = p.shape == PROBE_RUN ? n / 4 * 4 : n / tile * tile;
+    const int nb = blocks > 0 ? blocks : c->num_cus;   // default: one workgroup per compute unit
+    double b = 0.0;
+    for (int s = 0; s < count; ++s)
+        b += static_cast<double>(moved) * streams[s].elem_bytes * (streams[s].access == 3 ? 2 : 1);
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
+    const hipError_t e = launch_probe(p, nb, c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
+    if (bytes) *bytes = b;
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+const char* autoloco_build_id(void) { return AUTOLOCO_BUILD_ID; }
 
 int autoloco_alloc_spread(autoloco_ctx* c, int32_t count, size_t bytes, void** out, int32_t* spread) {
     if (c == nullptr) return AUTOLOCO_E_INVALID;

@@ -358,7 +358,7 @@ bool cfg_valid(const autoloco_controller_cfg& c) {
     if (c.n_ref_boot < 1 || c.n_ref_boot > kMaxList) return false;
     if (c.hist_max < 1 || c.hist_max > kMaxList) return false;
     if (c.n_var < 0 || c.moderate_confirm < 1 || c.fallback_count < 1) return false;
-    if (!(c.eps >= 0.0) || !(c.beta_tok >= 0.0 && c.beta_tok <= 1.0)) return false;
+    if (!(c.eps > 0.0) || !(c.beta_tok >= 0.0 && c.beta_tok <= 1.0)) return false;
     if (!(c.thr_cand <= c.thr_mod && c.thr_mod <= c.thr_sev)) return false;
     if (!(c.red_moderate > 1.0) || !(c.red_severe > 1.0)) return false;
     if (!(c.scale_floor > 0.0)) return false;
@@ -509,9 +509,21 @@ extern "C" int autoloco_controller_load(autoloco_controller* c, const void* buf,
     State tmp;
     std::memcpy(&tmp, buf, sizeof(State));
     if (tmp.magic != kMagic || tmp.version != kVersion || !cfg_valid(tmp.cfg)) return AUTOLOCO_E_INVALID;
-    if (tmp.n_hist < 0 || tmp.n_hist > tmp.cfg.hist_max || tmp.n_boot < 0 || tmp.n_boot > kMaxList ||
-        tmp.n_msamples < 0 || tmp.n_msamples > kMaxList || tmp.phase < 0 || tmp.phase > AUTOLOCO_PHASE_DONE)
+    // every count within the array it indexes (a reference interval is stored at
+    // boot[n_boot] before n_boot reaches n_ref_boot), every horizon within the
+    // configuration's bounds
+    const autoloco_controller_cfg& g = tmp.cfg;
+    auto horizon_ok = [&](int64_t h) { return h == g.h_base || (h >= g.h_min && h <= g.h_max); };
+    if (tmp.n_hist < 0 || tmp.n_hist > g.hist_max || tmp.n_boot < 0 || tmp.n_boot >= g.n_ref_boot ||
+        tmp.n_msamples < 0 || tmp.n_msamples > g.n_mapper_boot || tmp.phase < 0 || tmp.phase > AUTOLOCO_PHASE_DONE)
         return AUTOLOCO_E_INVALID;
+    if (!horizon_ok(tmp.h_acc) || !horizon_ok(tmp.h_cur) || tmp.h_step < 0 || tmp.start < 0 ||
+        tmp.start > g.budget_steps || tmp.var_count < 0 || tmp.mod_streak < 0 || tmp.bad_streak < 0 ||
+        tmp.interval < 0)
+        return AUTOLOCO_E_INVALID;
+    if ((tmp.phase == AUTOLOCO_PHASE_CAND1 || tmp.phase == AUTOLOCO_PHASE_CAND2) && !horizon_ok(tmp.h_cand))
+        return AUTOLOCO_E_INVALID;
+    if (tmp.bound_active && !horizon_ok(tmp.h_rej)) return AUTOLOCO_E_INVALID;
     c->s = tmp;
     return AUTOLOCO_OK;
 }

@@ -419,42 +419,6 @@ __global__ void __launch_bounds__(kBlock) round_kernel(RoundArgs a) {
     if constexpr (STATS) store_partials<NS, kBlock>(acc, a.partials);
 }
 
-// ------------------------------------------------------------ reset kernel --
-// theta_k <- theta for every replica.
-template <int K, int RT>
-__global__ void __launch_bounds__(kBlock) reset_kernel(RoundArgs a) {
-    constexpr int V = RT == RT_F32 ? 4 : 8;
-    const int64_t nvec = a.n / V;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (int64_t i = gtid; i < nvec; i += stride) {
-        const int64_t base = i * V;
-        if constexpr (RT == RT_F32) {
-            const f32x4 t = ld_f4(a.theta + base);
-#pragma unroll
-            for (int k = 0; k < K; ++k) st_f4(static_cast<float*>(a.replicas[k]) + base, t);
-        } else {
-            const f32x4 t0 = ld_f4(a.theta + base), t1 = ld_f4(a.theta + base + 4);
-            const u32x4 o = {bf16_pack(t0[0], t0[1]), bf16_pack(t0[2], t0[3]), bf16_pack(t1[0], t1[1]),
-                             bf16_pack(t1[2], t1[3])};
-#pragma unroll
-            for (int k = 0; k < K; ++k) st_u4(static_cast<uint16_t*>(a.replicas[k]) + base, o);
-        }
-    }
-    const int64_t tail0 = nvec * V;
-    if (gtid < a.n - tail0) {
-        const int64_t j = tail0 + gtid;
-        const float t = a.theta[j];
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if constexpr (RT == RT_F32)
-                static_cast<float*>(a.replicas[k])[j] = t;
-            else
-                static_cast<uint16_t*>(a.replicas[k])[j] = (uint16_t)bf16_rne(t);
-        }
-    }
-}
-
 // Launchers, one per (replica type, mode) translation unit.
 typedef hipError_t (*RoundLauncher)(int k, int blocks, hipStream_t stream, const RoundArgs& a);
 hipError_t launch_round_f32_m0(int, int, hipStream_t, const RoundArgs&);
@@ -475,7 +439,6 @@ hipError_t launch_round_bf16_m5(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m6(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m7(int, int, hipStream_t, const RoundArgs&);
 hipError_t launch_round_bf16_m8(int, int, hipStream_t, const RoundArgs&);
-hipError_t launch_reset(int rt, int k, int blocks, hipStream_t stream, const RoundArgs& a);
 // Resident workgroups per compute unit of the fused (update + stats + reset) kernel.
 int occupancy_round_f32_m4(int k);
 int occupancy_round_bf16_m4(int k);

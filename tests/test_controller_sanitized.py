@@ -3,7 +3,8 @@
 (`tests/c_abi/controller_from_c.c`) over every scripted scenario of the
 controller tests, with a checkpoint save / load every seventh interval: no
 sanitizer report, and every decision equal, field by field and bit for bit, to
-the library's (built without sanitizers)."""
+the library's (built without sanitizers).  Crafted checkpoints with counts or
+horizons out of range are refused under the same checks."""
 import ctypes as C
 import math
 import os
@@ -15,7 +16,7 @@ import pytest
 import paper_2609_36662_amd as al
 from paper_2609_36662_amd import _lib
 from tests.controller_driver import drive
-from tests.test_lib_host import SCENARIOS, _ccfg
+from tests.test_lib_host import CORRUPT_STATES, SCENARIOS, StateHead, _ccfg, saved_in_reference_bootstrap
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_36662_amd", "csrc")
@@ -80,3 +81,25 @@ def test_sanitized_controller_matches_library(exe, name):
     got = [_fields(_lib.Decision.from_buffer_copy(p.stdout[i:i + size])) for i in range(0, len(p.stdout), size)]
     bad = [i for i, (g, r) in enumerate(zip(got, ref)) if not _same(g, r)]
     assert not bad, f"decisions differ from interval {bad[0]}: {got[bad[0]]} vs {ref[bad[0]]}"
+
+
+@pytest.mark.parametrize("name", sorted(CORRUPT_STATES) + ["good"])
+def test_sanitized_checkpoint_load(exe, name):
+    # crafted checkpoints are refused before any field indexes an array; the
+    # good one loads and takes its next decision, with no sanitizer report
+    blob = saved_in_reference_bootstrap()
+    if name != "good":
+        field, value = CORRUPT_STATES[name]
+        setattr(StateHead.from_buffer(blob), field, value)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:halt_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
+    p = subprocess.run([exe, "load"], input=bytes(blob), capture_output=True, env=env, timeout=120)
+    err = p.stderr.decode(errors="replace")
+    assert p.returncode == 0, err[-3000:]
+    assert "runtime error" not in err and "Sanitizer" not in err, err[-3000:]
+    status = int.from_bytes(p.stdout[:4], "little", signed=True)
+    if name == "good":
+        assert status == 0 and int.from_bytes(p.stdout[4:8], "little", signed=True) == 0
+        d = _lib.Decision.from_buffer_copy(p.stdout[8:8 + C.sizeof(_lib.Decision)])
+        assert d.phase == 3
+    else:
+        assert status == -1 and len(p.stdout) == 4

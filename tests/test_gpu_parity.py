@@ -230,6 +230,27 @@ def test_largest_grid(ctx, n, k):
     assert_close_elementwise(dev.momentum.cpu().numpy(), ref.momentum, what="v'")
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("k", [1, 2, 8, 16])
+@pytest.mark.parametrize("n,grid", [(1, 0), (3, 0), (4 * 256 + 3, 0), (8 * 512 * 3 + 5, 3), (300_001, 0),
+                                    (300_001, 5)])
+def test_broadcast_reset_shapes(ctx, dtype, k, n, grid):
+    # the reset's window loop over ragged sizes, the last window shorter than one
+    # run per lane, and a capped grid that takes several grid-stride passes
+    inp = cpu_inputs(n, k, seed=23 + k, replica_dtype=dtype)
+    dev = to_device(inp)
+    al.autoloco_set_grid_limit(ctx, grid)
+    try:
+        al.autoloco_broadcast_reset(ctx, dev.theta, dev.replicas)
+        torch.cuda.synchronize()
+    finally:
+        al.autoloco_set_grid_limit(ctx, 0)
+    exp_bits = orr.reset_replicas(inp.theta.numpy(), 1, "f32" if dtype == torch.float32 else "bf16")[0]
+    for r in dev.replicas:
+        assert np.array_equal(host_array(r).view(np.uint8), exp_bits.view(np.uint8))
+    assert torch.equal(dev.theta.cpu(), inp.theta)
+
+
 def test_broadcast_reset(ctx):
     for dtype in (torch.float32, torch.bfloat16):
         n, k = 777_777, 5
@@ -267,7 +288,7 @@ def test_identical_replicas_zero_disagreement(ctx, k):
     assert st.C == pytest.approx(k * st.D / (st.D + EPS), rel=1e-12)
     # replicas equal to theta: D = 0, C = 0
     st0 = al.autoloco_round_stats(ctx, dev.theta, [dev.theta.clone() for _ in range(k)], EPS)
-    assert st0.D == 0.0 and st0.C == 0.0
+    assert st0.D == 0.0 and st0.C == 0.0 and st0.finite
 
 
 def test_plain_averaging_special_case(ctx):
@@ -309,7 +330,7 @@ def test_nonfinite_is_reported_not_fatal(ctx):
 
 
 # ------------------------------------------------------------ argument checks
-def _raw(ctx, theta, mom, reps, n, k, dtype=al.F32, flags=al.FUSE_STATS | al.FUSE_RESET):
+def _raw(ctx, theta, mom, reps, n, k, dtype=al.F32, flags=al.FUSE_STATS | al.FUSE_RESET, eps=EPS):
     import ctypes as C
     b = al._lib.Buffers()
     b.n, b.k, b.replica_dtype = n, k, dtype
@@ -318,7 +339,7 @@ def _raw(ctx, theta, mom, reps, n, k, dtype=al.F32, flags=al.FUSE_STATS | al.FUS
         b.replicas[i] = r
     st = al._lib.Stats()
     c = _tiny_coeffs(False)
-    return al.lib().autoloco_outer_step(ctx.handle, C.byref(b), C.byref(c), flags, EPS, C.byref(st))
+    return al.lib().autoloco_outer_step(ctx.handle, C.byref(b), C.byref(c), flags, eps, C.byref(st))
 
 
 def test_rejects_bad_arguments_without_touching_buffers(ctx):
@@ -338,12 +359,16 @@ def test_rejects_bad_arguments_without_touching_buffers(ctx):
     assert _raw(ctx, th, mo, [r0, r1], n, 2, dtype=7) == -1       # unknown dtype
     assert _raw(ctx, th, mo, [r0, r1], n, 2, flags=4) == -1       # unknown flag
     assert _raw(ctx, th, mo, [r0, r1], -1, 2) == -1               # negative n
+    for bad_eps in (0.0, -1e-12, float("nan"), float("inf")):    # eps > 0 (eq. adaptive-h-core-diagnostics)
+        assert _raw(ctx, th, mo, [r0, r1], n, 2, eps=bad_eps) == -1
     assert al.autoloco_last_error(ctx)                            # a message was left
     torch.cuda.synchronize()
     for t, s in zip([dev.theta, dev.momentum] + dev.replicas, snap):
         assert torch.equal(t, s)
     with pytest.raises(al.AutolocoError):
         al.autoloco_round_stats(ctx, dev.theta, [dev.theta], EPS)
+    with pytest.raises(al.AutolocoError):
+        al.autoloco_round_stats(ctx, dev.theta, dev.replicas, 0.0)
 
 
 def test_rejects_host_memory(ctx):

@@ -2,6 +2,7 @@
 header declares, and its host-side scalar code (schedule, learning-rate mass,
 outer correction, interval controller) takes exactly the oracle's values and
 decisions.  No device call is made here."""
+import ctypes as C
 import math
 import os
 import re
@@ -223,7 +224,7 @@ def test_controller_call_order_errors():
 
 def test_controller_rejects_bad_config():
     for bad in (dict(q_h=0), dict(h_min=800), dict(hist_max=17), dict(n_ref_boot=0),
-                dict(thr_cand=3.0), dict(red_severe=1.0)):
+                dict(thr_cand=3.0), dict(red_severe=1.0), dict(eps=0.0), dict(eps=-1e-12)):
         with pytest.raises(al.AutolocoError):
             al.autoloco_controller_create(al.default_controller_cfg(**bad))
 
@@ -256,6 +257,53 @@ def test_controller_checkpoint_resume_is_bitwise():
     bad[0] ^= 0xFF
     with pytest.raises(al.AutolocoError):
         al.autoloco_controller_load(resumed, bytes(bad))
+
+
+class StateHead(C.Structure):
+    """The leading fields of a saved controller state, in the library's layout
+    (checked against the magic and the configuration it holds)."""
+    _fields_ = [("magic", C.c_uint32), ("version", C.c_uint32), ("cfg", al._lib.ControllerCfg),
+                ("phase", C.c_int32), ("started", C.c_int32), ("start", C.c_int64), ("h_cur", C.c_int64),
+                ("h_step", C.c_int64), ("h_acc", C.c_int64), ("h_cand", C.c_int64), ("lambda_sel", C.c_double),
+                ("n_boot", C.c_int32), ("n_hist", C.c_int32)]
+
+
+def saved_in_reference_bootstrap():
+    """A checkpoint taken while the first reference interval is stored (phase
+    REF_BOOT, one of two reference intervals in)."""
+    cfg = oc.ControllerConfig()
+    ctl = al.autoloco_controller_create(_ccfg(cfg))
+    d = al.autoloco_select_interval(ctl, None)
+    for _ in range(2):
+        d = al.autoloco_select_interval(ctl, al.make_observation(1e-2, 4.0, 1.0, float(1 << 20) * d.h_step, d.h_step))
+    blob = bytearray(al.autoloco_controller_save(ctl))
+    head = StateHead.from_buffer(blob)
+    assert head.magic == 0x4C4F434F and head.cfg.h_base == cfg.h_base and head.cfg.n_ref_boot == 2
+    assert head.phase == 1 and head.n_boot == 1
+    return blob
+
+
+CORRUPT_STATES = {
+    "n_boot at the array end": ("n_boot", 16), "n_boot at n_ref_boot": ("n_boot", 2), "n_boot negative": ("n_boot", -1),
+    "n_hist above hist_max": ("n_hist", 17), "accepted horizon 0": ("h_acc", 0),
+    "accepted horizon above H_max": ("h_acc", 800), "current horizon huge": ("h_cur", 10 ** 9),
+    "negative steps": ("h_step", -5), "start past the budget": ("start", 50_001), "unknown phase": ("phase", 9),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CORRUPT_STATES))
+def test_controller_load_rejects_out_of_range_state(name):
+    field, value = CORRUPT_STATES[name]
+    blob = saved_in_reference_bootstrap()
+    setattr(StateHead.from_buffer(blob), field, value)
+    ctl = al.autoloco_controller_create()
+    with pytest.raises(al.AutolocoError) as e:
+        al.autoloco_controller_load(ctl, bytes(blob))
+    assert e.value.status == -1
+    # the good checkpoint still loads and completes the reference bootstrap
+    al.autoloco_controller_load(ctl, bytes(saved_in_reference_bootstrap()))
+    d = al.autoloco_select_interval(ctl, al.make_observation(1e-2, 4.0, 1.0, float(1 << 20) * 500, 500))
+    assert d.phase == 3                                   # variability intervals follow
 
 
 def test_device_calls_fail_loudly_without_a_gpu():
