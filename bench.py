@@ -147,16 +147,125 @@ def cpu_baseline(sample, coeffs, seconds: float, desc: str, threads: int = 1):
                       f"{done // n}x over {dt:.1f} s (numpy float64, {how})"}
 
 
+CPU_CHUNK = 1 << 24          # parameters per device-to-host chunk of the CPU baseline
+
+# A worker process's view of the shared chunk buffers: (theta, v, replicas, rdt).
+_SHARED = None
+
+
+def _attach(names, n, k, rdt):
+    """Worker initialiser: map the shared chunk buffers (numpy views)."""
+    import numpy as np
+    from multiprocessing import shared_memory
+    global _SHARED
+    shms = [shared_memory.SharedMemory(name=x) for x in names]
+    rt = np.float32 if rdt == "f32" else np.uint16
+    arr = [np.ndarray((n,), dtype=np.float32, buffer=shms[0].buf), np.ndarray((n,), dtype=np.float32, buffer=shms[1].buf)]
+    arr += [np.ndarray((n,), dtype=rt, buffer=m.buf) for m in shms[2:2 + k]]
+    _SHARED = (arr[0], arr[1], arr[2:], rdt, shms)
+
+
+def _oracle_part(job):
+    """The oracle's round (statistics, corrected step, reset) on [lo, hi) of the
+    shared chunk; returns the chunk part's sums."""
+    from oracle import round as orr
+    lo, hi, mu, eta, rho, normalize = job
+    th, mom, reps, rdt, _ = _SHARED
+    res = orr.sync_round(th[lo:hi], mom[lo:hi], [r[lo:hi] for r in reps], mu, eta, rho, normalize, 1e-12)
+    orr.reset_replicas(res.theta, len(reps), rdt)
+    return list(res.stats.sq_norm), list(res.stats.sq_dev), res.stats.sq_mean
+
+
+def cpu_procs(requested: int = 0) -> int:
+    """Worker processes of the CPU baseline: the cores this process may use
+    (sched_getaffinity), at most 16, the host share of one GPU on the
+    machines this runs on; `requested` > 0 overrides it."""
+    try:
+        p = len(os.sched_getaffinity(0))
+    except AttributeError:
+        p = os.cpu_count() or 1
+    return max(1, requested if requested > 0 else min(16, p))
+
+
+def make_cpu_pool(n, k, rdt, procs):
+    """Shared chunk buffers and a pool of worker processes started fresh
+    (spawn), before this process touches the GPU; returns (pool, buffers)."""
+    import multiprocessing as mp
+    from multiprocessing import shared_memory
+    c = min(n, CPU_CHUNK)
+    rb = 4 if rdt == "f32" else 2
+    shms = [shared_memory.SharedMemory(create=True, size=c * 4) for _ in range(2)]
+    shms += [shared_memory.SharedMemory(create=True, size=c * rb) for _ in range(k)]
+    names = [m.name for m in shms]
+    pool = mp.get_context("spawn").Pool(procs, initializer=_attach, initargs=(names, c, k, rdt)) if procs > 1 else None
+    _attach(names, c, k, rdt)                   # this process's own view (the one-core leg)
+    return pool, shms
+
+
+def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs):
+    """The float64 oracle, as it stands, over the whole workload.  The inputs
+    move device-to-host in chunks of 2^24 parameters into shared memory (not
+    timed); on each chunk the oracle runs once in this process (one core) and
+    once split over `procs` worker processes, and only that compute is timed.
+    The chunk sums are added in chunk order.  Returns the two legs and the
+    oracle's statistics of the whole workload."""
+    import numpy as np
+    import torch
+    from oracle import round as orr
+    pool, _ = pool_shms
+    th_s, mom_s, reps_s, _, _ = _SHARED
+    n, k = inp.theta.numel(), len(inp.replicas)
+    mu, eta, rho, nz = coeffs.mu, coeffs.eta_out, coeffs.rho, bool(coeffs.normalize)
+    s_tot, q_tot, m_tot = [0.0] * k, [0.0] * k, 0.0
+    t_one = t_par = 0.0
+    for c0 in range(0, n, CPU_CHUNK):
+        c1 = min(n, c0 + CPU_CHUNK)
+        m = c1 - c0
+        th_s[:m] = inp.theta[c0:c1].cpu().numpy()
+        mom_s[:m] = inp.momentum[c0:c1].cpu().numpy()
+        for dst, src in zip(reps_s, inp.replicas):
+            x = src[c0:c1].cpu()
+            dst[:m] = x.numpy() if rdt == "f32" else x.view(torch.int16).numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        one = _oracle_part((0, m, mu, eta, rho, nz))
+        t_one += time.perf_counter() - t0
+        step = -(-m // procs)
+        jobs = [(lo, min(m, lo + step), mu, eta, rho, nz) for lo in range(0, m, step)]
+        t0 = time.perf_counter()
+        parts = pool.map(_oracle_part, jobs) if pool is not None else [one]
+        t_par += time.perf_counter() - t0
+        for sn, sd, sm in parts:                # worker order within the chunk
+            s_tot = [a + b for a, b in zip(s_tot, sn)]
+            q_tot = [a + b for a, b in zip(q_tot, sd)]
+            m_tot += sm
+    stats = orr.finish_stats(s_tot, q_tot, m_tot, 1e-12)
+    nchunks = -(-n // CPU_CHUNK)
+    what = (f"{desc}: the whole workload, {n:,} parameters of every buffer, streamed device-to-host in "
+            f"{nchunks} chunks of up to {CPU_CHUNK:,} (transfer not timed); numpy float64 oracle")
+    par = {"value": n / t_par, "unit": "params/s", "cores": procs, "kind": "oracle",
+           "sample": what + (f", each chunk split over {procs} worker processes" if procs > 1 else ", one process"),
+           "seconds": t_par}
+    one_leg = {"value": n / t_one, "unit": "params/s", "cores": 1, "kind": "oracle",
+               "sample": what + ", one process on one core", "seconds": t_one}
+    return par, one_leg, stats
+
+
 def cpu_model() -> str:
-    """Model name of the host CPU (Linux), or "unknown"."""
+    """Model name of the host CPU with its family, model and stepping numbers
+    (Linux /proc/cpuinfo, first processor), or "unknown"."""
+    fields = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if not line.strip():
+                    break                      # first processor only
+                key, _, val = line.partition(":")
+                fields[key.strip()] = val.strip()
     except OSError:
-        pass
-    return "unknown"
+        return "unknown"
+    name = fields.get("model name", "unknown")
+    ids = [f"{k} {fields[k]}" for k in ("cpu family", "model", "stepping") if k in fields]
+    return f"{name} ({', '.join(ids)})" if ids else name
 
 
 def host_threads() -> int:
@@ -851,8 +960,13 @@ def main() -> int:
     ap.add_argument("--cpu-sample", type=int, default=1 << 22)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
-    ap.add_argument("--perturbed", type=int, default=20,
-                    help="extra rounds, each on freshly drawn replicas (drawn outside the timing)")
+    ap.add_argument("--back-to-back", type=int, default=20,
+                    help="round: also time this many rounds back to back on replicas already equal to theta'")
+    ap.add_argument("--no-plain", action="store_true", help="round: skip the plain-allocation comparison")
+    ap.add_argument("--cpu-procs", type=int, default=0,
+                    help="worker processes of the CPU baseline (0: the cores this process may use, at most 16)")
+    ap.add_argument("--perturbed", type=int, default=0,
+                    help="ignored (every timed round runs on freshly drawn replicas); kept so older commands run")
     ap.add_argument("--step", choices=("round", "inner", "share", "closed-loop", "probe", "reset"), default="round",
                     help="round: the synchronisation round; inner: one AdamW step of every worker; share: one "
                          "GPU's share of a round with one worker replica per GPU (K GPUs, no collectives); "
@@ -879,14 +993,20 @@ def main() -> int:
     if args.step == "closed-loop":
         return bench_closed_loop(args)
 
-    import torch
-    import paper_2609_36662_amd as al
-    from workloads import drift, shapes
-
+    from workloads import shapes
     shape_name, k, rdt, recipe_name, h_sel, h_base = WORKLOADS[args.workload]
     if args.k:
         k = args.k
     n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    # the CPU baseline's worker processes start before this process touches the GPU
+    pool = procs = None
+    if not args.no_cpu_baseline:
+        procs = cpu_procs(args.cpu_procs)
+        pool = make_cpu_pool(n, k, rdt, procs)
+
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift
     recipe = drift.MIXED if recipe_name == "mixed" else drift.spread_recipe(1e-3)
     tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
     s_r = 4 if rdt == "f32" else 2
@@ -915,14 +1035,6 @@ def main() -> int:
     log(f"buffers ({args.alloc}{', spread' if spread else ''}) allocated and inputs generated in "
         f"{time.perf_counter() - t:.1f} s")
 
-    sample = None
-    if not args.no_cpu_baseline:
-        s = min(n, args.cpu_sample)
-        import numpy as np
-        def host(tn):
-            x = tn[:s].cpu()
-            return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
-        sample = (host(inp.theta), host(inp.momentum), [host(r) for r in inp.replicas], rdt)
 
     if args.grid:
         al.autoloco_set_grid_limit(ctx, args.grid)
@@ -959,29 +1071,33 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} rounds); grid {blocks} x {threads}")
 
-    kernel_ms = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        _, ms = one_round()
-        kernel_ms.append(ms)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall / args.steps * 1e3
-    log(f"timed {args.steps} rounds: {ms_per_step:.3f} ms/round wall, kernel mean "
-        f"{statistics.mean(kernel_ms):.3f} ms")
-
-    perturbed_ms, perturbed_wall = [], []
-    for i in range(args.perturbed):
+    # Exactly `steps` timed rounds, each on freshly drawn replicas (drawn
+    # untimed before it) and bracketed by device synchronisations; the call
+    # itself returns once the sums are on the host.
+    kernel_ms, round_ms = [], []
+    for i in range(args.steps):
         drift.fill_replicas(inp, seed=1000 + i, recipe=recipe)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        _, ms = one_round()                      # blocks until the sums are on the host
-        perturbed_wall.append((time.perf_counter() - t1) * 1e3)
-        perturbed_ms.append(ms)
-    if perturbed_ms:
-        log(f"{len(perturbed_ms)} rounds on freshly drawn replicas: kernel {statistics.median(perturbed_ms):.3f} ms, "
-            f"round {statistics.median(perturbed_wall):.3f} ms (medians)")
+        _, ms = one_round()
+        torch.cuda.synchronize()
+        round_ms.append((time.perf_counter() - t1) * 1e3)
+        kernel_ms.append(ms)
+    ms_per_step = statistics.mean(round_ms)
+    log(f"timed {args.steps} rounds on freshly drawn replicas: {ms_per_step:.3f} ms/round wall (mean), kernel mean "
+        f"{statistics.mean(kernel_ms):.3f} ms")
+
+    # the same rounds back to back, every replica already equal to theta' (the
+    # kernel has no data-dependent control flow: the same time)
+    b2b_ms = None
+    if args.back_to_back:
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.back_to_back):
+            one_round()
+        torch.cuda.synchronize()
+        b2b_ms = (time.perf_counter() - t1) / args.back_to_back * 1e3
+        log(f"{args.back_to_back} rounds back to back: {b2b_ms:.3f} ms/round")
 
     ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
 
@@ -1007,16 +1123,47 @@ def main() -> int:
     tag = f"round_{rdt}_k{k}_{args.workload}" + ("" if args.codec == "fp32" else f"_{args.codec}")
     traffic = committed_traffic(tag, INT8_SOURCES if args.codec == "int8" else None)
 
+    # The same round on plain torch allocations (consecutive buffers, adjacent in
+    # physical memory), for comparison with the spread placement above.
+    plain = None
+    if args.alloc == "spread" and not args.no_plain and args.codec == "fp32":
+        alt = drift.empty_inputs(n, k, replica_dtype=tdtype, device=dev)
+        drift.fill_theta_momentum(alt, seed=42, recipe=recipe)
+        pk, pw = [], []
+        for i in range(6):
+            drift.fill_replicas(alt, seed=2000 + i, recipe=recipe)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            al.autoloco_outer_step(ctx, alt.theta, alt.momentum, alt.replicas, coeffs, flags, 1e-12)
+            torch.cuda.synchronize()
+            if i:
+                pw.append((time.perf_counter() - t1) * 1e3)
+                pk.append(al.autoloco_last_kernel_ms(ctx))
+        del alt
+        torch.cuda.empty_cache()
+        plain = {"ms_per_round_mean": statistics.mean(pw), "kernel_ms_mean": statistics.mean(pk),
+                 "achieved_gbs": bytes_per_round / (statistics.mean(pk) * 1e-3) / 1e9, "rounds": len(pw),
+                 "alloc": "torch (consecutive allocations)"}
+        log(f"plain allocations: {plain['ms_per_round_mean']:.3f} ms/round, kernel {plain['kernel_ms_mean']:.3f} ms "
+            f"({plain['achieved_gbs']:.0f} GB/s)")
+
     cpu = cpu1 = None
-    if sample is not None:
+    if pool is not None:
+        # fresh inputs for the oracle (the timed rounds left every replica at theta')
+        drift.fill_replicas(inp, seed=3000, recipe=recipe)
+        torch.cuda.synchronize()
+        gst = al.autoloco_round_stats(ctx, inp.theta, inp.replicas, 1e-12)
         desc = f"{args.workload} K={k} {rdt}"
-        p = host_threads()
-        log(f"timing the oracle on the CPU sample: one thread, then {p} threads")
-        cpu1 = cpu_baseline(sample, coeffs, args.cpu_seconds, desc)
-        cpu = cpu_baseline(sample, coeffs, args.cpu_seconds, desc, threads=p) if p > 1 else cpu1
-        for leg in {id(cpu): cpu, id(cpu1): cpu1}.values():
+        log(f"timing the oracle over the whole workload: one core, then {procs} processes")
+        cpu, cpu1, ost = cpu_baseline_stream(inp, coeffs, rdt, desc, pool, procs)
+        match = all(abs(a - b) <= 1e-4 * abs(b) for a, b in ((gst.D, ost.D), (gst.C, ost.C),
+                                                             (gst.disagreement, ost.disagreement)))
+        log(f"oracle over the whole workload: D {ost.D:.9g} C {ost.C:.9g} (GPU D {gst.D:.9g} C {gst.C:.9g}, "
+            f"{'within' if match else 'OUTSIDE'} 1e-4)")
+        for leg in (cpu, cpu1):
             leg["cpu_model"] = cpu_model()
             leg["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / leg["value"]
+            leg["statistics_match_gpu_within_1e-4"] = match
 
     out = {
         "metric": metric_name(METRIC, args, k),
@@ -1046,11 +1193,14 @@ def main() -> int:
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
         },
+        "timing": "mean of the timed rounds, each on freshly drawn replicas and bracketed by device "
+                  "synchronisations (the call returns once the statistics are on the host)",
         "kernel_ms_mean": mean_ms,
         "kernel_ms_min": min(kernel_ms),
-        "kernel_ms_perturbed_median": statistics.median(perturbed_ms) if perturbed_ms else None,
-        "round_ms_perturbed_median": statistics.median(perturbed_wall) if perturbed_wall else None,
-        "perturbed_rounds": len(perturbed_ms),
+        "kernel_ms_median": statistics.median(kernel_ms),
+        "round_ms_median": statistics.median(round_ms),
+        "round_ms_back_to_back": b2b_ms,
+        "plain_alloc": plain,
         "copy_ceiling_gbs": ceiling,
         "traffic_reference": reference,
         "first_round_stats": {k2: first_stats[k2] for k2 in ("D", "C", "disagreement", "finite")}
@@ -1060,6 +1210,13 @@ def main() -> int:
         "kernel_source_sha256_16": kernel_source_hash(INT8_SOURCES if args.codec == "int8" else None),
     }
     print(json.dumps(out), flush=True)
+    if pool is not None:
+        if pool[0] is not None:
+            pool[0].close()
+            pool[0].join()
+        for shm in pool[1]:
+            shm.close()
+            shm.unlink()
     del inp
     if args.alloc == "spread":
         del ts

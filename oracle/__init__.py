@@ -34,12 +34,15 @@ Modules
 
 Parity unpinned (no value printed by the paper and no closed form fixes them;
 each is one reading of a point the paper leaves open):
-  * the robust scale floor and MAD consistency factor used for z_max,
-  * the coefficient of the log-space EMA of the reference diagnostics,
+  * the constants 1.4826 (MAD consistency factor) and 1e-3 (scale floor) of
+    z_max's robust scale,
+  * the coefficient 0.9 of the log-space EMA of the reference diagnostics,
   * tie-breaking of reductions and geometric midpoints,
-  * the count of severe/invalid intervals that triggers the H_min fallback,
-  * the rejected-horizon bound and reduction paths beyond their printed
-    constants.
-The adaptive-interval controller is otherwise pinned by the executed interval
-sequence the paper prints for its C4 run (App. F.2).
+  * the count 2 of severe/invalid intervals that triggers the H_min fallback,
+  * the rejected-horizon bound beyond its printed constants.
+The forms around those constants (the median/MAD scale over odd and even
+histories, the log-space EMA and which intervals update it, the fallback after
+a streak versus a single reduction) are pinned by hand-derived scenarios in the
+test suite, and the controller as a whole by the executed interval sequence the
+paper prints for its C4 run (App. F.2).
 """

@@ -35,3 +35,38 @@ def test_metric_names_the_workload_it_measured():
     assert bench.metric_name(bench.CLOSED_LOOP_METRIC, a, 4, True).endswith("(% of peak), 1M params K=4, 5 rounds")
     a = types.SimpleNamespace(workload="llama-7b", steps=20)
     assert bench.metric_name(bench.CLOSED_LOOP_METRIC, a, 4, True) == bench.CLOSED_LOOP_METRIC
+
+
+def test_streamed_cpu_baseline_equals_one_oracle_pass():
+    # the CPU baseline's chunked, multi-process oracle pass over a workload gives
+    # the statistics of one oracle pass over all of it (float64, chunk order)
+    import numpy as np
+    import torch
+    sys.path.insert(0, ROOT)
+    import bench
+    import paper_2609_36662_amd as al
+    from oracle import round as orr
+    from workloads import drift
+    old = bench.CPU_CHUNK
+    bench.CPU_CHUNK = 1 << 14
+    try:
+        for rdt, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+            n, k = 3 * (1 << 14) + 13, 4
+            pool = bench.make_cpu_pool(n, k, rdt, 2)
+            try:
+                inp = drift.make_round_inputs(n, k, seed=5, device="cpu", replica_dtype=dt)
+                coeffs = al.make_coeffs(0.85, 1.5, 1.49, True)
+                par, one, st = bench.cpu_baseline_stream(inp, coeffs, rdt, "check", pool, 2)
+            finally:
+                pool[0].close()
+                pool[0].join()
+                for shm in pool[1]:
+                    shm.close()
+                    shm.unlink()
+            reps = [r.numpy() if rdt == "f32" else r.view(torch.int16).numpy().view(np.uint16) for r in inp.replicas]
+            ref = orr.sync_round(inp.theta.numpy(), inp.momentum.numpy(), reps, 0.85, 1.5, 1.49, True, 1e-12)
+            for a, b in ((st.D, ref.stats.D), (st.C, ref.stats.C), (st.disagreement, ref.stats.disagreement)):
+                assert abs(a - b) <= 1e-12 * abs(b)
+            assert par["cores"] == 2 and one["cores"] == 1 and "4 chunks" in par["sample"]
+    finally:
+        bench.CPU_CHUNK = old

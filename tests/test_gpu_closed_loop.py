@@ -11,15 +11,23 @@ per-worker part by 10, so coherence collapses and the interval must be
 assessed severe and the horizon must shrink (a reduction, or the return from a
 rejected candidate).
 
-* Small size (N = 262,147, K = 4): the oracle runs its own loop (float64
-  rounds, Python controller) on the same drift draws; statistics, parameters
-  and every decision must agree.
+* Small size (N = 262,147, K = 4): every round the oracle (float64 round,
+  Python controller) restarts from the GPU's fp32 theta, v and endpoints, so
+  theta' and v' meet 1e-5 (|o| + rms) and the statistics 1e-4 in every round;
+  each controller takes its own side's statistics and the decisions must be
+  identical, with z_max within the bound that the observed statistics
+  differences imply.
 * Llama-style 7B (N = 6,738,415,616, K = 4 fp32, 162 GB resident), 20 rounds:
   every round's θ', v' and reset replicas are checked against the oracle on
   sampled parameters, the statistics against the App. C.1 identity and bounds,
-  and in two rounds a 1/256 sub-range against a full oracle pass.
+  and in two rounds a 1/256 sub-range against a full oracle pass; the oracle
+  controller runs in lockstep on the GPU's statistics, and on those statistics
+  moved to each corner of their 1e-4 band, and takes the library's decision
+  every time.
 """
+import copy
 import math
+import warnings
 
 import numpy as np
 import pytest
@@ -65,7 +73,24 @@ def _cpu_drift(n, k, r, scale, fault):
     return out
 
 
+def _z_bound(d_log_d, d_log_c, z):
+    """How far the controller's z_max can move when every D it has seen is off
+    by at most d_log_d in log space and every C by d_log_c (eqs.
+    adaptive-h-core-residuals and adaptive-h-core-deviation): r_D moves by at
+    most d_log_d (half the log of D and half the log of its reference, a
+    log-space mean of earlier D), r_C by 2 d_log_c, so every residual in a
+    history by dr = max(d_log_d, 2 d_log_c); its median by dr, its MAD by 2 dr,
+    its scale by 1.4826 * 2 dr, and z = [r - c]_+ / s, with s >= 1e-3, by at
+    most (2 dr + 2.9652 dr z) / 1e-3."""
+    dr = max(d_log_d, 2.0 * d_log_c)
+    return (2.0 * dr + 2.9652 * dr * z) / 1e-3 * (1.0 + 1e-6) + 1e-12
+
+
 def test_closed_loop_small_matches_oracle(ctx):
+    # Every round the oracle restarts from the GPU's own fp32 theta, v and
+    # endpoints, so theta', v' and the statistics meet the plain bars in every
+    # round (no error carried over from earlier rounds); the two controllers
+    # take their own statistics, and their decisions must agree.
     n, k = 262_147, 4
     ctl_o = oc.OracleController(oc.ControllerConfig())
     ctl_g = al.autoloco_controller_create()
@@ -73,14 +98,12 @@ def test_closed_loop_small_matches_oracle(ctx):
     dec_g = al.autoloco_select_interval(ctl_g, None)
 
     gen = torch.Generator().manual_seed(42)
-    theta0 = (torch.randn(n, generator=gen) * 0.02).numpy().astype(np.float32)
-    mom0 = (torch.randn(n, generator=gen) * 1e-4).numpy().astype(np.float32)
-    th_o, v_o = theta0.astype(np.float64), mom0.astype(np.float64)
-    th_g = torch.from_numpy(theta0).cuda()
-    v_g = torch.from_numpy(mom0).cuda()
+    th_g = (torch.randn(n, generator=gen) * 0.02).cuda()
+    v_g = (torch.randn(n, generator=gen) * 1e-4).cuda()
     reps_g = [torch.empty(n, device="cuda") for _ in range(k)]
     lam1 = dec_o.lambda_sel
     fault_done = False
+    d_log_d = d_log_c = 0.0
     for r in range(ROUNDS):
         assert (dec_g.start_step, dec_g.h_tok, dec_g.h_step, dec_g.h_ref, dec_g.phase) == \
             (dec_o.start_step, dec_o.h_tok, dec_o.h_step, dec_o.h_ref, dec_o.phase), r
@@ -89,20 +112,19 @@ def test_closed_loop_small_matches_oracle(ctx):
         lam = dec_o.lambda_sel
         fault = not fault_done and r >= FAULT_FROM and dec_o.phase in ASSESSED
         d = _cpu_drift(n, k, r, lam / lam1, fault)
-        # GPU endpoints: its own theta plus the same drift (rounded to fp32); oracle: float64
         for kk in range(k):
             reps_g[kk].copy_(th_g + torch.from_numpy(d[kk].astype(np.float32)).cuda())
-        reps_o = [th_o + dd for dd in d]
+        th_o, v_o = host_array(th_g).astype(np.float64), host_array(v_g).astype(np.float64)
+        reps_o = [host_array(x).astype(np.float64) for x in reps_g]
         st = al.autoloco_outer_step(ctx, th_g, v_g, reps_g, dec_g.coeffs, al.FUSE_STATS | al.FUSE_RESET, EPS)
         ref = orr.sync_round(th_o, v_o, reps_o, dec_o.coeffs.mu, dec_o.coeffs.eta, dec_o.coeffs.rho,
                              dec_o.coeffs.normalize, EPS)
-        # fp32 endpoints perturb each pseudo-gradient by at most half an fp32 ulp of theta
-        # (~1e-9 against a ~1e-3 drift), hence the slightly wider statistics bar
-        assert_stats_close(st, ref.stats, tol=2e-4)
-        th_o, v_o = ref.theta, ref.momentum
-        assert_close_elementwise(th_g.cpu().numpy(), th_o, tol=1e-5 * (r + 1), what=f"theta' round {r}")
-        assert_close_elementwise(v_g.cpu().numpy(), v_o, tol=1e-5 * (r + 1), what=f"v' round {r}")
+        assert_stats_close(st, ref.stats)
+        assert_close_elementwise(host_array(th_g), ref.theta, what=f"theta' round {r}")
+        assert_close_elementwise(host_array(v_g), ref.momentum, what=f"v' round {r}")
         assert all(torch.equal(x, th_g) for x in reps_g)
+        d_log_d = max(d_log_d, abs(math.log(st.D / ref.stats.D)))
+        d_log_c = max(d_log_c, abs(math.log(st.C / ref.stats.C)))
         tokens = TOKENS_PER_STEP * dec_o.h_step
         h_fault = dec_o.h_tok
         dec_o = ctl_o.select_interval(oc.Observation(ref.stats.D, ref.stats.C, lam, tokens, dec_o.h_step,
@@ -110,16 +132,22 @@ def test_closed_loop_small_matches_oracle(ctx):
         dec_g = al.autoloco_select_interval(ctl_g, al.make_observation(st.D, st.C, lam, tokens, dec_g.h_step,
                                                                        st.finite))
         assert dec_g.assessment == dec_o.assessment, r
-        assert (math.isnan(dec_g.z_max) and math.isnan(dec_o.z_max)) or \
-            dec_g.z_max == pytest.approx(dec_o.z_max, rel=1e-3, abs=1e-3), r
-        if not math.isnan(dec_o.z_max):
+        if math.isnan(dec_o.z_max):
+            assert math.isnan(dec_g.z_max), r
+        else:
+            bound = _z_bound(d_log_d, d_log_c, dec_o.z_max)
+            assert abs(dec_g.z_max - dec_o.z_max) <= bound, (r, dec_g.z_max, dec_o.z_max, bound)
+            # the class is decided by z, so it must not sit within that bound of a threshold
             for thr in (1.5, 2.5, 4.0):
-                assert abs(dec_o.z_max - thr) > 1e-6, f"near-tie z at round {r}: {dec_o.z_max}"
+                if abs(dec_o.z_max - thr) <= bound:
+                    warnings.warn(f"near-tie z at round {r}: {dec_o.z_max} within {bound:.3g} of {thr}")
         if fault:
             fault_done = True
             assert dec_o.assessment == oc.Assessment.SEVERE
             assert dec_o.h_tok < h_fault
     assert fault_done
+    # the statistics of the two sides agree far inside their 1e-4 bar
+    assert d_log_d < 1e-6 and d_log_c < 1e-6, (d_log_d, d_log_c)
 
 
 def _gather(t, idx):
@@ -148,6 +176,8 @@ def test_closed_loop_7b_twenty_rounds(ctx):
     drift.fill_theta_momentum(inp, seed=42)
     ctl = al.autoloco_controller_create()
     dec = al.autoloco_select_interval(ctl, None)
+    ctl_o = oc.OracleController(oc.ControllerConfig())      # the oracle controller in lockstep
+    dec_o = ctl_o.select_interval(None)
     lam1 = dec.lambda_sel
     rng = np.random.default_rng(7)
     edge = np.array([0, 1, 2, 3, (1 << 31) - 1, 1 << 31, (1 << 32) + 5, n - 4, n - 3, n - 2, n - 1])
@@ -181,9 +211,21 @@ def test_closed_loop_7b_twenty_rounds(ctx):
         assert st.finite and st.disagreement == pytest.approx(st.D - st.sq_mean, rel=1e-4)
         assert 0.0 <= st.C <= k * st.D / (st.D + EPS)
         h_fault = dec.h_tok
-        dec = al.autoloco_select_interval(ctl, al.make_observation(st.D, st.C, lam, TOKENS_PER_STEP * dec.h_step,
-                                                                   dec.h_step, st.finite))
-        print(f"round {r}: h_step {dec.h_step} D {st.D:.6g} C {st.C:.6g} assessment {dec.assessment}", flush=True)
+        tokens, h_done = TOKENS_PER_STEP * dec.h_step, dec.h_step
+        # the oracle controller on the same statistics, and on the statistics moved
+        # to every corner of their +-1e-4 band: the same decision each time
+        decide = lambda c_, d_, cc_: c_.select_interval(oc.Observation(d_, cc_, lam, tokens, h_done, st.finite))
+        corners = [decide(copy.deepcopy(ctl_o), st.D * (1 + a), st.C * (1 + b), ) for a in (-1e-4, 1e-4)
+                   for b in (-1e-4, 1e-4)]
+        dec_o = decide(ctl_o, st.D, st.C)
+        dec = al.autoloco_select_interval(ctl, al.make_observation(st.D, st.C, lam, tokens, h_done, st.finite))
+        for x in [dec_o] + corners:
+            assert (x.start_step, x.h_tok, x.h_step, x.h_ref, x.assessment, x.phase) == \
+                (dec.start_step, dec.h_tok, dec.h_step, dec.h_ref, dec.assessment, dec.phase), r
+            assert (x.coeffs.mu, x.coeffs.eta, x.coeffs.rho) == (dec.coeffs.mu, dec.coeffs.eta_out, dec.coeffs.rho), r
+        assert (math.isnan(dec.z_max) and math.isnan(dec_o.z_max)) or dec.z_max == dec_o.z_max, r
+        print(f"round {r}: h_step {dec.h_step} D {st.D:.6g} C {st.C:.6g} assessment {dec.assessment} "
+              f"z {dec.z_max:.4g}", flush=True)
         if fault:
             fault_done = True
             assert dec.assessment == oc.Assessment.SEVERE
