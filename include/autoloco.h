@@ -234,6 +234,33 @@ int autoloco_outer_step_bf16(autoloco_ctx* ctx, const autoloco_buffers* bufs,
                              const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
                              autoloco_stats* out, uint16_t* mean_bf16);
 
+/* The corrected outer step of autoloco_outer_step, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): no context, and no allocation of any kind
+ * (no hipMalloc, no pinned host memory).  The statistics' reduction scratch
+ * (per-workgroup partial sums and the final sums: 1,024 workgroups x 33 sums
+ * plus 33, 270 KB) is a static device array of the library, one copy per
+ * device, held until the process ends; the first call on a device looks up its
+ * address with that device current.  The call runs the kernels, launch shape
+ * and reduction order of autoloco_outer_step on the same device, so theta',
+ * v', the replicas and the statistics equal that call's bit for bit.
+ *   device: HIP device ordinal (the call makes it current and restores the
+ *     previous one); stream: a hipStream_t of that device, or NULL.
+ *   bufs, coeffs, flags, eps, out: as autoloco_outer_step.  With FUSE_STATS the
+ *     sums are copied to the calling thread's stack and the call waits for
+ *     them; without it the call only launches kernels on the stream.
+ * Every call on a device uses that device's one array, and each call writes
+ * every word of it that it reads, so nothing needs clearing between calls;
+ * calls that overlap in time on one device (from several threads or streams)
+ * race on the array and give wrong statistics: serialise them.
+ * Errors: E_INVALID (as autoloco_outer_step, a bad device ordinal, or a launch
+ * shape of more than 1,024 workgroups, which a device of more than 341
+ * compute units would need below k = 8), E_ALIGN, E_ALIAS, E_DEVICE.  There is
+ * no context, so no message is kept. */
+int autoloco_outer_step_static(int device, void* stream, const autoloco_buffers* bufs,
+                               const autoloco_outer_coeffs* coeffs, uint32_t flags, double eps,
+                               autoloco_stats* out);
+
 /* Replica reset alone: theta_k <- theta for every replica (Alg. "AutoLoCo
  * outer interval", start of the local loop).  Asynchronous on the stream.
  * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */

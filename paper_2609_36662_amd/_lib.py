@@ -144,6 +144,8 @@ SYMBOLS = [
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p, C.c_void_p]),
     ("autoloco_outer_step_bf16", C.c_int, [C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
                                            C.c_uint32, C.c_double, C.POINTER(Stats), C.c_void_p]),
+    ("autoloco_outer_step_static", C.c_int, [C.c_int, C.c_void_p, C.POINTER(Buffers), C.POINTER(OuterCoeffs),
+                                             C.c_uint32, C.c_double, C.POINTER(Stats)]),
     ("autoloco_broadcast_reset", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_traffic_reference", C.c_int, [C.c_void_p, C.POINTER(Buffers)]),
     ("autoloco_traffic_probe", C.c_int, [C.c_void_p, C.c_int64, C.POINTER(ProbeStream), C.c_int32, C.c_int32,
@@ -424,6 +426,26 @@ def autoloco_outer_step(ctx: Context, theta, momentum, replicas, coeffs: OuterCo
                                      C.byref(out) if flags & FUSE_STATS else None),
            "autoloco_outer_step", ctx)
     return out if flags & FUSE_STATS else None
+
+
+def autoloco_outer_step_static(theta, momentum, replicas, coeffs: OuterCoeffs, flags: int = FUSE_STATS | FUSE_RESET,
+                               eps: float = 1e-12, device: Optional[int] = None, stream=None, n=None) -> Optional[Stats]:
+    """autoloco_outer_step without a context: the library allocates nothing
+    (its reduction scratch is a static device array)."""
+    import torch
+    b = make_buffers(theta, replicas, momentum, n)
+    if device is None:
+        device = theta.device.index if theta.device.index is not None else torch.cuda.current_device()
+    if stream is None:
+        # an ordinal torch does not know goes to the library as is (it rejects it)
+        stream = torch.cuda.current_stream(device) if 0 <= device < torch.cuda.device_count() else 0
+    raw = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    st = Stats()
+    status = lib().autoloco_outer_step_static(int(device), C.c_void_p(raw), C.byref(b), C.byref(coeffs),
+                                              int(flags), float(eps), C.byref(st))
+    if status != 0:
+        raise AutolocoError(status, "autoloco_outer_step_static")
+    return st if flags & FUSE_STATS else None
 
 
 def autoloco_outer_step_int8(ctx: Context, theta, momentum, replicas, coeffs: OuterCoeffs,

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -30,7 +31,18 @@ namespace {
 
 constexpr int kMaxBlocks = 16384;   // scratch sized for this many workgroups
 
+// Workgroups whose partial sums the static scratch below holds: the default
+// grid is one workgroup per compute unit from K = 8 and three below it (768 on
+// MI355X).
+constexpr int kStaticBlocks = 1024;
+
 }  // namespace
+
+// Reduction scratch of autoloco_outer_step_static on every device: per-workgroup
+// partial sums [kStaticBlocks][33], then the 33 final sums (270 KB).  In host
+// code the name stands for the variable, not for its device address: host code
+// uses only the address hipGetSymbolAddress returns with the device current.
+static __device__ __align__(256) double scratch[kStaticBlocks * kMaxSums + kMaxSums];
 
 struct autoloco_ctx {
     int device = 0;
@@ -416,9 +428,84 @@ void zero_stats(int k, double eps, autoloco_stats* out) {
     finish_stats(z, k, eps, out);
 }
 
+// ---------------------------------------------- outer step without allocation
+constexpr int kStaticDevices = 64;
+
+// Per device, set up on its first call: scratch's device address and the
+// tables the launch shape is computed from (those of a context).
+struct StaticDevice {
+    bool ready = false;
+    double* scratch_ptr = nullptr;   // scratch's device address on this device
+    int num_cus = 0;
+    int occupancy[2][AUTOLOCO_MAX_K + 1] = {};
+};
+StaticDevice g_static[kStaticDevices];
+std::mutex g_static_mu;
+
+// With `device` current.
+int static_device(int device, StaticDevice** out) {
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    StaticDevice& d = g_static[device];
+    if (!d.ready) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return AUTOLOCO_E_DEVICE;
+        }
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
+            return AUTOLOCO_E_DEVICE;
+        d.scratch_ptr = static_cast<double*>(p);
+        d.num_cus = cus > 0 ? cus : 1;
+        for (int k = 1; k <= AUTOLOCO_MAX_K; ++k) {
+            d.occupancy[0][k] = occupancy_round_f32_m4(k);
+            d.occupancy[1][k] = occupancy_round_bf16_m4(k);
+        }
+        d.ready = true;
+    }
+    *out = &d;
+    return AUTOLOCO_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int autoloco_outer_step_static(int device, void* stream, const autoloco_buffers* b, const autoloco_outer_coeffs* co,
+                               uint32_t flags, double eps, autoloco_stats* out) {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count || device >= kStaticDevices)
+        return AUTOLOCO_E_INVALID;
+    DeviceGuard g(device);
+    if (!g.ok) return AUTOLOCO_E_DEVICE;
+    StaticDevice* sd = nullptr;
+    int st = static_device(device, &sd);
+    if (st != AUTOLOCO_OK) return st;
+    // a context on the stack over the static scratch: the same validation,
+    // launch shape and kernels as autoloco_outer_step, nothing allocated
+    autoloco_ctx c;
+    c.device = device;
+    c.stream = static_cast<hipStream_t>(stream);
+    c.num_cus = sd->num_cus;
+    std::memcpy(c.occupancy, sd->occupancy, sizeof(c.occupancy));
+    c.partials = sd->scratch_ptr;
+    c.sums = sd->scratch_ptr + kStaticBlocks * kMaxSums;
+    double host_sums[kMaxSums];
+    c.host_sums = host_sums;
+    bool stats = false, reset = false;
+    st = validate_step(&c, b, co, flags, eps, out, &stats, &reset);
+    if (st != AUTOLOCO_OK) return st;
+    if (b->n == 0) {
+        if (stats) zero_stats(b->k, eps, out);
+        return AUTOLOCO_OK;
+    }
+    if (blocks_for(&c, b->n, b->replica_dtype, b->k) > kStaticBlocks) return AUTOLOCO_E_INVALID;
+    RoundArgs a = make_args(&c, b);
+    set_step(a, co);
+    const int mode = stats ? (reset ? MODE_UPDATE_STATS_RESET : MODE_UPDATE_STATS)
+                           : (reset ? MODE_UPDATE_RESET : MODE_UPDATE);
+    return run_round(&c, b, a, mode, stats, eps, out);
+}
 
 int autoloco_create(int device, void* stream, autoloco_ctx** out) {
     if (out == nullptr) return AUTOLOCO_E_INVALID;
