@@ -542,7 +542,7 @@ def bench_share(args) -> int:
     refs = {
         "payload": ([(theta, R), (rep, R), (payload, W)], al.PROBE_RUN2, args.grid or 2 * num_cus),
         "shard_step": ([(theta[:ns], RW), (v_shard, RW)] + [(r, R) for r in recv] + [(mean, W)], al.PROBE_RUN2,
-                       args.grid or 2 * num_cus),
+                       args.grid or 3 * num_cus),
         # the reset alone runs three workgroups per compute unit
         "reset": ([(theta, R), (rep, W)], al.PROBE_RUN1 if rdt == "f32" else al.PROBE_RUN2,
                   args.grid or 3 * num_cus),
@@ -558,7 +558,7 @@ def bench_share(args) -> int:
     log("traffic references: " + ", ".join(f"{k_} {v:.3f} ms" for k_, v in ref_ms.items()))
     achieved = b_payload / (tp * 1e-3) / 1e9
     ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
-    traffic = committed_traffic(f"share_{rdt}_k{k}_{args.workload}", SHARE_SOURCES)
+    traffic = committed_traffic(f"share_{rdt}_k{k}_{args.workload}_payload", SHARE_SOURCES)
     out = {
         "metric": SHARE_METRIC,
         "value": n / (ms_per_step * 1e-3),
@@ -664,7 +664,8 @@ def bench_reset(args) -> int:
         "config": {"workload": f"{args.workload}: theta ({n:,} fp32) into K={k} {rdt} replicas",
                    "n_params": n, "k": k, "bytes": nbytes, "alloc": alloc_label("spread", spread)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "reset_kernel"},
+                     "frac": achieved / PEAK_HBM_GBS, "kernel": "reset_kernel",
+                     "traffic": committed_traffic(f"reset_{rdt}_k{k}_{args.workload}", RESET_SOURCES)},
         "kernel_ms_median": ms, "traffic_reference_ms_median": ref_ms, "ratio_to_reference": ms / ref_ms,
         "copy_ceiling_gbs": ceiling, "cpu_baseline": None,
         "kernel_source_sha256_16": kernel_source_hash(RESET_SOURCES),

@@ -382,10 +382,12 @@ int run_one_sum(autoloco_ctx* c, Launch launch, int blocks, double* out) {
 }
 
 // Workgroups of the per-GPU share kernels (two quads of 4 parameters per lane
-// per window): two per CU at most (measured at 1.1B / 8 shards on MI355X: 512
-// workgroups 7-9 % faster than 768, 2,048 and more 15-90 % slower).
-int blocks8(const autoloco_ctx* ctx, int64_t n) {
-    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * 2;
+// per window): the payload kernel two per CU, the shard step three (measured on
+// MI355X with both kernels loading both runs before any store: payload 1.1B
+// 1.93 ms at 512 against 1.98 at 768; shard step 3B K = 8 2.27 ms at 768 against
+// 2.40 at 512, 2.31 at 1,024, and equal at 1.1B).
+int blocks8(const autoloco_ctx* ctx, int64_t n, int per_cu = 2) {
+    int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * per_cu;
     if (limit > kMaxBlocks) limit = kMaxBlocks;
     int64_t want = (n / 8 + kBlock - 1) / kBlock;
     if (want < 1) want = 1;
@@ -984,7 +986,7 @@ int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const 
     a.scale = co->normalize ? static_cast<float>(1.0 / co->rho) : 1.0f;
     a.inv_k64 = 1.0 / static_cast<double>(b->k);
     a.partials = c->partials;
-    const int blocks = blocks8(c, b->n);
+    const int blocks = blocks8(c, b->n, 3);
     const int k = b->k;
     return run_one_sum(c, [&] { return launch_shard_step(k, blocks, c->stream, a); }, blocks, sq_mean);
 }

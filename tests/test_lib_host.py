@@ -313,3 +313,27 @@ def test_device_calls_fail_loudly_without_a_gpu():
         pytest.skip("a GPU is visible")
     with pytest.raises(RuntimeError):
         al.autoloco_create(0)
+
+
+def test_library_carries_the_hash_of_its_sources():
+    from paper_2609_36662_amd import build
+    assert al.autoloco_build_id() == build.source_hash()
+
+
+def test_stale_library_is_refused(tmp_path):
+    import shutil
+    from paper_2609_36662_amd import _lib, build
+    # the hash covers every source file: one changed byte in a kernel header changes it
+    root = tmp_path / "tree"
+    for rel in ("include", "paper_2609_36662_amd/csrc"):
+        shutil.copytree(os.path.join(ROOT, rel), root / rel)
+    shutil.copy(os.path.join(ROOT, "paper_2609_36662_amd", "build.py"), root / "paper_2609_36662_amd" / "build.py")
+    assert build.source_hash(str(root)) == build.source_hash()
+    hdr = root / "paper_2609_36662_amd" / "csrc" / "round_kernels.hpp"
+    hdr.write_text(hdr.read_text() + "\n")
+    stale = build.source_hash(str(root))
+    assert stale != build.source_hash()
+    # a library whose id differs from the sources beside it is refused
+    with pytest.raises(RuntimeError, match="built from other sources"):
+        _lib.check_build_id(al.lib(), stale)
+    _lib.check_build_id(al.lib(), build.source_hash())
