@@ -98,55 +98,6 @@ def committed_traffic(tag: str, sources=None):
         return None
 
 
-def cpu_baseline(sample, coeffs, seconds: float, desc: str, threads: int = 1):
-    """The float64 oracle, as it stands, on a bounded sample of the workload.
-
-    The sample is cut into 16 fixed chunks that run through the oracle one
-    after another, or with ``threads`` > 1 on a pool of threads (numpy releases
-    the interpreter lock inside its array operations); the chunks' sums are
-    combined in chunk order."""
-    import numpy as np
-    from concurrent.futures import ThreadPoolExecutor
-    from oracle import round as orr
-    th, mom, reps, rdt = sample
-    n = th.shape[0]
-    k = len(reps)
-    step = -(-n // 16)
-    bounds = [(lo, min(n, lo + step)) for lo in range(0, n, step)]
-
-    def chunk(lo_hi):
-        lo, hi = lo_hi
-        res = orr.sync_round(th[lo:hi], mom[lo:hi], [r[lo:hi] for r in reps], coeffs.mu, coeffs.eta_out,
-                             coeffs.rho, bool(coeffs.normalize), 1e-12)
-        orr.reset_replicas(res.theta, k, rdt)
-        return res.stats
-
-    def one_round(pool):
-        parts = list(pool.map(chunk, bounds)) if pool is not None else [chunk(b) for b in bounds]
-        s = [sum(p.sq_norm[i] for p in parts) for i in range(k)]
-        q = [sum(p.sq_dev[i] for p in parts) for i in range(k)]
-        return orr.finish_stats(s, q, sum(p.sq_mean for p in parts), 1e-12)
-
-    pool = ThreadPoolExecutor(threads) if threads > 1 else None
-    try:
-        done = 0
-        t0 = time.perf_counter()
-        while True:
-            one_round(pool)
-            done += n
-            if time.perf_counter() - t0 >= seconds:
-                break
-        dt = time.perf_counter() - t0
-    finally:
-        if pool is not None:
-            pool.shutdown()
-    del np
-    how = "16 chunks on one thread" if threads == 1 else f"16 chunks on {threads} threads"
-    return {"value": done / dt, "unit": "params/s", "cores": threads, "kind": "oracle",
-            "sample": f"{desc}: first {n:,} parameters of every buffer, round repeated "
-                      f"{done // n}x over {dt:.1f} s (numpy float64, {how})"}
-
-
 CPU_CHUNK = 1 << 24          # parameters per device-to-host chunk of the CPU baseline
 
 # A worker process's view of the shared chunk buffers: (theta, v, replicas, rdt).
@@ -202,13 +153,27 @@ def make_cpu_pool(n, k, rdt, procs):
     return pool, shms
 
 
-def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs):
+def close_cpu_pool(pool_shms) -> None:
+    """Stop the worker processes and release the shared chunk buffers."""
+    if pool_shms is None:
+        return
+    pool, shms = pool_shms
+    if pool is not None:
+        pool.close()
+        pool.join()
+    for shm in shms:
+        shm.close()
+        shm.unlink()
+
+
+def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs, one_core=True):
     """The float64 oracle, as it stands, over the whole workload.  The inputs
     move device-to-host in chunks of 2^24 parameters into shared memory (not
-    timed); on each chunk the oracle runs once in this process (one core) and
-    once split over `procs` worker processes, and only that compute is timed.
-    The chunk sums are added in chunk order.  Returns the two legs and the
-    oracle's statistics of the whole workload."""
+    timed); on each chunk the oracle runs once in this process (one core, when
+    `one_core` is set or there is no pool) and once split over `procs` worker
+    processes, and only that compute is timed.  The chunk sums are added in
+    chunk order.  Returns the two legs (the one-core leg None when skipped) and
+    the oracle's statistics of the whole workload."""
     import numpy as np
     import torch
     from oracle import round as orr
@@ -226,9 +191,10 @@ def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs):
         for dst, src in zip(reps_s, inp.replicas):
             x = src[c0:c1].cpu()
             dst[:m] = x.numpy() if rdt == "f32" else x.view(torch.int16).numpy().view(np.uint16)
-        t0 = time.perf_counter()
-        one = _oracle_part((0, m, mu, eta, rho, nz))
-        t_one += time.perf_counter() - t0
+        if one_core or pool is None:
+            t0 = time.perf_counter()
+            one = _oracle_part((0, m, mu, eta, rho, nz))
+            t_one += time.perf_counter() - t0
         step = -(-m // procs)
         jobs = [(lo, min(m, lo + step), mu, eta, rho, nz) for lo in range(0, m, step)]
         t0 = time.perf_counter()
@@ -238,6 +204,8 @@ def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs):
             s_tot = [a + b for a, b in zip(s_tot, sn)]
             q_tot = [a + b for a, b in zip(q_tot, sd)]
             m_tot += sm
+        if (c0 // CPU_CHUNK) % 64 == 63:
+            log(f"oracle: {c1:,} of {n:,} parameters, {t_par:.1f} s of oracle time so far")
     stats = orr.finish_stats(s_tot, q_tot, m_tot, 1e-12)
     nchunks = -(-n // CPU_CHUNK)
     what = (f"{desc}: the whole workload, {n:,} parameters of every buffer, streamed device-to-host in "
@@ -246,7 +214,8 @@ def cpu_baseline_stream(inp, coeffs, rdt, desc, pool_shms, procs):
            "sample": what + (f", each chunk split over {procs} worker processes" if procs > 1 else ", one process"),
            "seconds": t_par}
     one_leg = {"value": n / t_one, "unit": "params/s", "cores": 1, "kind": "oracle",
-               "sample": what + ", one process on one core", "seconds": t_one}
+               "sample": what + ", one process on one core", "seconds": t_one} \
+        if one_core or pool is None else None
     return par, one_leg, stats
 
 
@@ -835,14 +804,21 @@ def bench_closed_loop(args) -> int:
     controller must answer with a shorter horizon.  A timed step runs from the
     synchronisation before the round to the decision for the next interval."""
     import math
-    import torch
-    import paper_2609_36662_amd as al
-    from workloads import drift, shapes
+    from workloads import shapes
 
     shape_name, k, rdt = WORKLOADS[args.workload][0], WORKLOADS[args.workload][1], WORKLOADS[args.workload][2]
     if args.k:
         k = args.k
     n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
+    # the CPU baseline's worker processes start before this process touches the GPU
+    pool = procs = None
+    if not args.no_cpu_baseline:
+        procs = cpu_procs(args.cpu_procs)
+        pool = make_cpu_pool(n, k, rdt, procs)
+
+    import torch
+    import paper_2609_36662_amd as al
+    from workloads import drift
     tdtype = torch.float32 if rdt == "f32" else torch.bfloat16
     s_r = 4 if rdt == "f32" else 2
     bytes_per_round = n * (2 * k * s_r + 16)
@@ -864,20 +840,18 @@ def bench_closed_loop(args) -> int:
     assessed = (4, 5, 6)   # autoloco_phase: monitoring and the two candidate phases
     fault_done = False
     walls, kms, trace = [], [], []
-    sample = None
+    cpu = ost = None
     for r in range(args.warmup + args.steps):
         lam = dec.lambda_sel
         fault = not fault_done and r >= 12 and dec.phase in assessed
         jit = math.exp(0.05 * math.sin(1.7 * r + 0.3)) * (10.0 if fault else 1.0)
         drift.fill_replicas(inp, seed=100 + r, scale=lam / lam1, indep_scale=[jit] * k)
-        if r == args.warmup and not args.no_cpu_baseline:
-            import numpy as np
-            m = min(n, args.cpu_sample)
-
-            def host(tn):
-                x = tn[:m].cpu()
-                return x.view(torch.int16).numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.numpy()
-            sample = ((host(inp.theta), host(inp.momentum), [host(x) for x in inp.replicas], rdt), dec.coeffs)
+        if r == args.warmup and pool is not None:
+            # untimed: the oracle over this round's whole state, with the decision's coefficients
+            torch.cuda.synchronize()
+            log(f"timing the oracle over the whole state of round {r} on {procs} processes")
+            cpu, _, ost = cpu_baseline_stream(inp, dec.coeffs, rdt, f"{args.workload} K={k} {rdt} closed loop, "
+                                              f"round {r}", pool, procs, one_core=False)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         st = al.autoloco_outer_step(ctx, inp.theta, inp.momentum, inp.replicas, dec.coeffs,
@@ -888,6 +862,12 @@ def bench_closed_loop(args) -> int:
         wall = (time.perf_counter() - t0) * 1e3
         if fault:
             fault_done = True
+        if r == args.warmup and cpu is not None:
+            match = all(abs(a - b) <= 1e-4 * abs(b) for a, b in ((st.D, ost.D), (st.C, ost.C),
+                                                                 (st.disagreement, ost.disagreement)))
+            log(f"oracle on round {r}: D {ost.D:.9g} C {ost.C:.9g} (GPU D {st.D:.9g} C {st.C:.9g}, "
+                f"{'within' if match else 'OUTSIDE'} 1e-4)")
+            cpu["statistics_match_gpu_within_1e-4"] = match
         if r >= args.warmup:
             walls.append(wall)
             kms.append(al.autoloco_last_kernel_ms(ctx))
@@ -898,11 +878,7 @@ def bench_closed_loop(args) -> int:
     ms_per_step = statistics.mean(walls)
     mean_ms = statistics.mean(kms)
     achieved = bytes_per_round / (mean_ms * 1e-3) / 1e9
-    cpu = None
-    if sample is not None:
-        log(f"timing the oracle on the CPU sample ({host_threads()} threads)")
-        cpu = cpu_baseline(sample[0], sample[1], args.cpu_seconds, f"{args.workload} K={k} {rdt} closed loop",
-                           threads=host_threads())
+    if cpu is not None:
         cpu["cpu_model"] = cpu_model()
         cpu["gpu_speedup"] = (n / (ms_per_step * 1e-3)) / cpu["value"]
     tag = f"round_{rdt}_k{k}_{args.workload}"
@@ -937,6 +913,7 @@ def bench_closed_loop(args) -> int:
         "kernel_source_sha256_16": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
+    close_cpu_pool(pool)
     del inp, ts
     ctx.close()
     return 0
@@ -1211,13 +1188,7 @@ def main() -> int:
         "kernel_source_sha256_16": kernel_source_hash(INT8_SOURCES if args.codec == "int8" else None),
     }
     print(json.dumps(out), flush=True)
-    if pool is not None:
-        if pool[0] is not None:
-            pool[0].close()
-            pool[0].join()
-        for shm in pool[1]:
-            shm.close()
-            shm.unlink()
+    close_cpu_pool(pool)
     del inp
     if args.alloc == "spread":
         del ts

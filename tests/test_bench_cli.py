@@ -57,16 +57,14 @@ def test_streamed_cpu_baseline_equals_one_oracle_pass():
                 inp = drift.make_round_inputs(n, k, seed=5, device="cpu", replica_dtype=dt)
                 coeffs = al.make_coeffs(0.85, 1.5, 1.49, True)
                 par, one, st = bench.cpu_baseline_stream(inp, coeffs, rdt, "check", pool, 2)
+                par2, none, st2 = bench.cpu_baseline_stream(inp, coeffs, rdt, "check", pool, 2, one_core=False)
             finally:
-                pool[0].close()
-                pool[0].join()
-                for shm in pool[1]:
-                    shm.close()
-                    shm.unlink()
+                bench.close_cpu_pool(pool)
             reps = [r.numpy() if rdt == "f32" else r.view(torch.int16).numpy().view(np.uint16) for r in inp.replicas]
             ref = orr.sync_round(inp.theta.numpy(), inp.momentum.numpy(), reps, 0.85, 1.5, 1.49, True, 1e-12)
             for a, b in ((st.D, ref.stats.D), (st.C, ref.stats.C), (st.disagreement, ref.stats.disagreement)):
                 assert abs(a - b) <= 1e-12 * abs(b)
             assert par["cores"] == 2 and one["cores"] == 1 and "4 chunks" in par["sample"]
+            assert none is None and par2["cores"] == 2 and (st2.D, st2.C) == (st.D, st.C)
     finally:
         bench.CPU_CHUNK = old
