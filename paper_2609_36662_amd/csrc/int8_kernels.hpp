@@ -13,8 +13,8 @@
 //   Q_k += (Delta_k - Delta_agg)^2, M += Delta_agg^2          C uses the aggregate
 //   corrected Nesterov step with Delta_agg, reset of the replicas
 // The two block maxima (the K worker maxima, then the mean's) are exact and
-// order-independent: a wavefront max over DPP lane exchanges, then the waves
-// through LDS, with one barrier each.
+// order-independent: lane exchanges (DPP) inside each wavefront, then the
+// waves through LDS, with one barrier each.
 // Every codec step runs in fp32 with IEEE division and round-to-nearest-even,
 // so the codes are the same integers the FP32 definition gives.
 #pragma once
@@ -50,33 +50,36 @@ __device__ __forceinline__ float codec_scale(float amax) {
 // Codes of x[0..NV) at scale s (r = fp32(1/s)): the integers nearest
 // fp32(x / s), ties to even, clipped to +-127.  t = x * r differs from
 // fp32(x / s) by at most (3u + u^2) |x / s| <= 2.28e-5 here (u = 2^-24,
-// |x / s| <= 127.00003; the test's own rounding, fused or not, adds at most
-// 3e-8), so rint(t) is the same integer unless t lies within 3e-5 of a
-// half-integer; only then (about 6e-5 of the elements) is the IEEE quotient
-// formed.  The test runs for every element first and the quotients are taken
-// behind one wavefront-uniform branch, entered only when some lane of the
-// wavefront needs one, so the common path has no per-element branch.
+// |x / s| <= 127.00003), so rint(t) is the same integer unless t lies within
+// 3e-5 of a half-integer; only then (about 6e-5 of the elements) is the IEEE
+// quotient formed.  t - rint(t) is exact (Sterbenz); where the compiler fuses
+// the product into it, the test value is x r - rint(t) rounded once, within
+// u |x / s| of the exact one, which the margin covers as well.  The common path
+// has no per-element test: each lane keeps the largest |t - rint(t)| of its
+// elements, and one wavefront-uniform branch leads to the quotients when some
+// lane's exceeds the bound.  A NaN t drops out of that maximum, which is
+// harmless: t is NaN only when x is NaN, or infinite in a block whose scale is
+// infinite (r = 0), and the quotient is NaN then too.
 // The clip is implied by the scale and costs no instruction: s is the block's
 // largest magnitude over 127 rounded once (or the larger 2^-126), so |t| and
 // |fp32(x / s)| are at most 127 (1 + 3 * 2^-24) < 127.5 for every x of the
 // block, and their nearest integers lie in [-127, 127].  (A non-finite block
-// has a NaN or infinite scale and decodes to non-finite values either way.)
+// has an infinite scale and decodes to non-finite values either way.)
 // x(e) gives element e (evaluated again on the rare path).
 template <int NV, typename X>
 __device__ __forceinline__ void codec_q(X x, float s, float r, float (&q)[NV]) {
-    // t may lie too close to a half-integer (also true for NaN)
-    auto near_half = [](float t, float qi) { return !(fabsf(t - qi) < 0.5f - 3.0e-5f); };
-    bool any = false;
+    constexpr float kNear = 0.5f - 3.0e-5f;
+    float dev = 0.0f;
 #pragma unroll
     for (int e = 0; e < NV; ++e) {
         const float t = x(e) * r;
         q[e] = __builtin_rintf(t);
-        any = any || near_half(t, q[e]);
+        dev = fmaxf(dev, fabsf(t - q[e]));
     }
-    if (__builtin_amdgcn_ballot_w64(any) != 0) {
+    if (__builtin_amdgcn_ballot_w64(dev >= kNear) != 0) {
 #pragma unroll
         for (int e = 0; e < NV; ++e)
-            if (near_half(x(e) * r, q[e])) q[e] = __builtin_rintf(x(e) / s);
+            if (!(fabsf(x(e) * r - q[e]) < kNear)) q[e] = __builtin_rintf(x(e) / s);
     }
 }
 
@@ -120,6 +123,54 @@ __device__ __forceinline__ void block_max(float (&v)[NV], uint32_t* lds) {
     }
 }
 
+// Block maxima of up to 8 workers' non-negative values (compared as their bit
+// patterns) over a workgroup of NW waves; returns worker (lane mod 8)'s in
+// every lane.  Instead of one wavefront reduction per worker, a halving
+// exchange inside each group of 8 lanes (partners 7 - i, i ^ 1, i ^ 2; every
+// lane sends the half of its values its partner keeps) leaves lane i with the
+// group's maximum of worker w(i) = 4 b2 + 2 b0 + b1 (b_j the bits of i), a
+// rotation by 8 lanes joins the two groups of each row of 16, and every wave
+// stores its 4 row values per worker.  After the one barrier each lane reads
+// the 4 NW values of its worker (rows 16-byte aligned, 4 words apart in bank
+// order, so the 8 workers' reads fall in distinct banks).  The same reuse rule
+// as block_max holds for the LDS region.
+constexpr int kWorkerMaxStride(int nw) { return 4 * nw + 4; }
+template <int K, int NW>
+__device__ __forceinline__ float worker_block_max(const float (&v)[K], uint32_t* lds) {
+    static_assert(K <= 8, "at most 8 workers");
+    constexpr int S = kWorkerMaxStride(NW);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t m[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m[j] = j < K ? __float_as_uint(v[j]) : 0u;
+    const bool lo = (lane & 4) == 0, even = (lane & 1) == 0, b1 = (lane & 2) != 0;
+    uint32_t a4[4], a2[2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {   // partner 7 - i (row_half_mirror): the low lane keeps workers 0..3
+        const uint32_t send = lo ? m[j + 4] : m[j], keep = lo ? m[j] : m[j + 4];
+        a4[j] = max(keep, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, 0x141, 0xF, 0xF, false));
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {   // partner i ^ 1 (quad_perm 1,0,3,2)
+        const uint32_t send = even ? a4[j + 2] : a4[j], keep = even ? a4[j] : a4[j + 2];
+        a2[j] = max(keep, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, 0xB1, 0xF, 0xF, false));
+    }
+    uint32_t c;
+    {                               // partner i ^ 2 (quad_perm 2,3,0,1)
+        const uint32_t send = b1 ? a2[0] : a2[1], keep = b1 ? a2[1] : a2[0];
+        c = max(keep, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)send, 0x4E, 0xF, 0xF, false));
+    }
+    c = max(c, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)c, 0x128, 0xF, 0xF, false));   // row_ror:8
+    const int w = (lane & 4) + ((lane & 1) << 1) + ((lane & 2) >> 1);
+    if ((lane & 8) == 0) lds[w * S + wave * 4 + (lane >> 4)] = c;
+    __syncthreads();
+    const uint32_t* p = lds + (lane & 7) * S;
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < 4 * NW; ++i) r = max(r, p[i]);
+    return __uint_as_float(r);
+}
+
 constexpr int kInt8Threads = 512;  // one codec block of 4,096 parameters per workgroup
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -135,9 +186,10 @@ struct BoolC {
 // every load and store is a whole vector; the one shorter last block, if any,
 // goes through a second instance of the same body with per-element accesses.
 // The next block of a workgroup is loaded while the current one is encoded:
-// up to 8 bf16 workers its raw replica words and theta go to registers (the
-// block barriers wait for LDS traffic only), and pseudo-gradients are formed
-// from the raw words where they are used, which leaves the registers for it;
+// up to 8 bf16 workers its raw replica words, theta and momentum go to
+// registers (the block barriers wait for LDS traffic only), pseudo-gradients
+// are formed from the raw words where they are used, and each thread's fp64
+// sums live in LDS slots of its own, which leaves the registers for it;
 // up to 8 fp32 workers its theta and replica vectors go straight to LDS
 // (global_load_lds_dwordx4, no registers), each wave into pieces only it reads
 // back, behind an explicit count of the vector memory instructions issued
@@ -157,15 +209,31 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     constexpr bool LP = RT == RT_F32 && K <= 8;
     constexpr int NW = NT / 64;
     constexpr int KW = RT == RT_BF16 ? K : 1;   // raw bf16 replica words held per thread
-    __shared__ uint32_t lds_max[NT / 64 * K];   // worker block maxima
+    // worker block maxima
+    __shared__ uint32_t lds_max[K <= 8 ? 8 * kWorkerMaxStride(NT / 64) : NT / 64 * K];
     __shared__ uint32_t lds_mmax[NT / 64];      // the mean's block maximum
     // prefetched vectors, [stream (theta, replica 0..K-1)][run][wave][lane];
     // every wave reads back only the 1 KB pieces it loaded itself
     __shared__ f32x4 lds_pf[LP ? (K + 1) * G * NT : 1];
 
-    double acc[NS];
+    // per-thread fp64 sums: in registers, or with the bf16 prefetch (which holds
+    // many registers) in this thread's own LDS slots, [sum][thread]
+    constexpr bool AL = PF;
+    double acc[AL ? 1 : NS];
+    __shared__ double lds_acc[AL ? NS * NT : 1];
+    auto acc_add = [&](int j, double x) {
+        if constexpr (AL)
+            lds_acc[j * NT + threadIdx.x] += x;
+        else
+            acc[j] += x;
+    };
 #pragma unroll
-    for (int j = 0; j < NS; ++j) acc[j] = 0.0;
+    for (int j = 0; j < NS; ++j) {
+        if constexpr (AL)
+            lds_acc[j * NT + threadIdx.x] = 0.0;
+        else
+            acc[j] = 0.0;
+    }
 
     const int64_t nfull = a.n / kCodecBlock;
     const int64_t nblocks = (a.n + kCodecBlock - 1) / kCodecBlock;
@@ -188,13 +256,14 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
     };
 
-    // bf16: raw words (two per run) and theta of one block (full: vector loads;
-    // else per element, zero beyond n)
+    // bf16: raw words (two per run), theta and (full blocks) momentum of one
+    // block (full: vector loads; else per element, zero beyond n)
     // two register sets for the bf16 prefetch: the loop takes blocks in pairs and
     // the sets swap roles (current / next) instead of being copied
     u32x2 wA[KW][G], wB[PF ? KW : 1][G];
     float tA[V], tB[PF ? V : 1];
-    auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto full_c) {
+    float mA[PF || LP ? V : 1], mB[PF ? V : 1];
+    auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto& m, auto full_c) {
         constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -203,6 +272,11 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 const f32x4 t4 = ld_f4(a.theta + o);
 #pragma unroll
                 for (int e = 0; e < W; ++e) t[g * W + e] = t4[e];
+                if constexpr (PF) {
+                    const f32x4 m4 = ld_f4(a.momentum + o);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) m[g * W + e] = m4[e];
+                }
 #pragma unroll
                 for (int k = 0; k < KW; ++k)
                     w[k][g] = __builtin_nontemporal_load(
@@ -223,7 +297,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
     };
 
-    auto body = [&](int64_t blk, auto full_c, auto& cw, auto& cth, auto& nw, auto& nth) {
+    auto body = [&](int64_t blk, auto full_c, auto& cw, auto& cth, auto& cm, auto& nw, auto& nth, auto& nm) {
         constexpr bool FULL = decltype(full_c)::value;
         int64_t off[G];
         int valid[G];
@@ -243,8 +317,12 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
 
         float th[V], v[V], d[RT == RT_F32 ? K : 1][V];
         if constexpr (RT == RT_BF16) {
-            // momentum first: the update waits for it, and in-order completion
-            // then leaves the prefetch below in flight
+            // momentum: from the prefetch, or loaded first (the update waits for
+            // it, and in-order completion then leaves the loads below in flight)
+            if constexpr (PF && FULL) {
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[e] = cm[e];
+            } else
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int64_t o = off[g];
@@ -261,9 +339,9 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 // next full block of this workgroup; on its last one, this block again
                 // (every iteration issues the same loads)
                 const int64_t nb = blk + gridDim.x < nfull ? blk + gridDim.x : blk;
-                load_bf16(nb, nw, nth, BoolC<true>{});
+                load_bf16(nb, nw, nth, nm, BoolC<true>{});
             } else {
-                load_bf16(blk, cw, cth, full_c);
+                load_bf16(blk, cw, cth, cm, full_c);
             }
 #pragma unroll
             for (int e = 0; e < V; ++e) th[e] = cth[e];
@@ -277,20 +355,29 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 // outstanding" imply the loads have landed in LDS.
                 constexpr int after = G * (2 + (RESET ? K : 0));
                 __builtin_amdgcn_s_waitcnt((after & 0xF) | ((after >> 4) << 14) | 0x70 | 0xF00);
+                // momentum: this block's was loaded in the previous iteration; the
+                // next block's is loaded now, ahead of the direct loads below (so
+                // the count above never includes it, wherever the compiler puts it)
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[e] = cm[e];
+                const int64_t nb = blk + gridDim.x < nfull ? blk + gridDim.x : blk;
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const f32x4 m4 = ld_f4(a.momentum + nb * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) cm[g * W + e] = m4[e];
+                }
             }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int64_t o = off[g];
                 if constexpr (FULL && LP) {
                     // theta and the replicas from the LDS prefetch (complete: see the
-                    // wait at the end of the loop body), momentum from memory
+                    // wait above)
                     const int lane = threadIdx.x & 63;
-                    const f32x4 t4 = pf_piece(0, g)[lane], v4 = ld_f4(a.momentum + o);
+                    const f32x4 t4 = pf_piece(0, g)[lane];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        th[g * W + e] = t4[e];
-                        v[g * W + e] = v4[e];
-                    }
+                    for (int e = 0; e < 4; ++e) th[g * W + e] = t4[e];
 #pragma unroll
                     for (int k = 0; k < K; ++k) {
                         const f32x4 r4 = pf_piece(k + 1, g)[lane];
@@ -347,7 +434,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 float s = 0.f;
 #pragma unroll
                 for (int e = 0; e < V; ++e) s = __builtin_fmaf(D(k, e), D(k, e), s);
-                acc[k] += (double)s;
+                acc_add(k, (double)s);
             }
         }
 
@@ -360,7 +447,11 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
             for (int e = 0; e < V; ++e) m = fmaxf(m, fabsf(D(k, e)));
             amax[k] = m;
         }
-        block_max<K, NT>(amax, lds_max);
+        float am_lane = 0.0f;   // up to 8 workers: worker (lane mod 8)'s block maximum
+        if constexpr (K <= 8)
+            am_lane = worker_block_max<K, NT / 64>(amax, lds_max);
+        else
+            block_max<K, NT>(amax, lds_max);
 
         // The K scales and their reciprocals are the same in every lane: lane k
         // computes worker k's (one IEEE division of each kind for all workers
@@ -368,9 +459,12 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         float scale_k[K], recip_k[K];
         {
             const int lane = threadIdx.x & 63;
-            float am = amax[0];
+            float am = am_lane;
+            if constexpr (K > 8) {
+                am = amax[0];
 #pragma unroll
-            for (int k = 1; k < K; ++k) am = lane == k ? amax[k] : am;
+                for (int k = 1; k < K; ++k) am = lane == k ? amax[k] : am;
+            }
             const float sv = codec_scale(am);
             const float rv = 1.0f / sv;
 #pragma unroll
@@ -441,12 +535,12 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                     const float t = D(k, e) - agg[e];
                     q = __builtin_fmaf(t, t, q);
                 }
-                acc[K + k] += (double)q;
+                acc_add(K + k, (double)q);
             }
             float m = 0.f;
 #pragma unroll
             for (int e = 0; e < V; ++e) m = __builtin_fmaf(agg[e], agg[e], m);
-            acc[2 * K] += (double)m;
+            acc_add(2 * K, (double)m);
         }
 
         // corrected Nesterov step with the decoded aggregate, and the reset
@@ -503,29 +597,47 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     };
 
     if constexpr (PF) {
-        if (blockIdx.x < nfull) load_bf16(blockIdx.x, wA, tA, BoolC<true>{});
+        if (blockIdx.x < nfull) load_bf16(blockIdx.x, wA, tA, mA, BoolC<true>{});
         // the first block's words are complete before the loop
         __builtin_amdgcn_s_waitcnt(0);
         // blocks in pairs: the first of a pair prefetches into B, the second into A
         for (int64_t blk = blockIdx.x; blk < nfull; blk += 2 * (int64_t)gridDim.x) {
-            body(blk, BoolC<true>{}, wA, tA, wB, tB);
+            body(blk, BoolC<true>{}, wA, tA, mA, wB, tB, mB);
             if (blk + gridDim.x >= nfull) break;
-            body(blk + gridDim.x, BoolC<true>{}, wB, tB, wA, tA);
+            body(blk + gridDim.x, BoolC<true>{}, wB, tB, mB, wA, tA, mA);
         }
     } else {
         if constexpr (LP) {
-            if (blockIdx.x < nfull) pf_issue(blockIdx.x);
+            if (blockIdx.x < nfull) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const f32x4 m4 = ld_f4(a.momentum + (int64_t)blockIdx.x * kCodecBlock + g * (kCodecBlock / 2) +
+                                           (int64_t)threadIdx.x * W);
+#pragma unroll
+                    for (int e = 0; e < W; ++e) mA[g * W + e] = m4[e];
+                }
+                pf_issue(blockIdx.x);
+            }
             __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
         }
-        for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{}, wA, tA, wB, tB);
+        for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{}, wA, tA, mA, wB, tB, mB);
         // the last iteration's direct loads (a re-read, unused) land before anything
         // else uses this workgroup's LDS or the workgroup ends
         if constexpr (LP) __builtin_amdgcn_s_waitcnt(0);
     }
     // the shorter last block belongs to the workgroup the grid stride gives it
-    if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{}, wA, tA, wB, tB);
+    if (nfull < nblocks && nfull % gridDim.x == blockIdx.x) body(nfull, BoolC<false>{}, wA, tA, mA, wB, tB, mB);
 
-    if constexpr (STATS) store_partials<NS, NT>(acc, a.partials);
+    if constexpr (STATS) {
+        if constexpr (AL) {
+            double r[NS];
+#pragma unroll
+            for (int j = 0; j < NS; ++j) r[j] = lds_acc[j * NT + threadIdx.x];
+            store_partials<NS, NT>(r, a.partials);
+        } else {
+            store_partials<NS, NT>(acc, a.partials);
+        }
+    }
 }
 
 typedef hipError_t (*Int8Launcher)(int k, int blocks, hipStream_t stream, const Int8Args& a);

@@ -76,26 +76,43 @@ def test_prefetch_wait_covers_the_direct_loads(asm, st, rs):
         # the direct loads of the next block are issued inside the loop, after the LDS reads
         dma = [i for i in range(h, len(body)) if "global_load_lds" in body[i]]
         assert len([i for i in dma if i < h + 1000]) >= 2 * (k + 1), (k, "direct loads missing")
-        # the loop is rotated: the block that falls into the header ends the iteration;
-        # every branch back into the loop goes there, and it holds at least n stores
-        tail = max(i for i in range(h) if re.match(r"^\.LBB\d+_\d+:", body[i]))
-        label = body[tail].split(":")[0]
-        back = [i for i, l in enumerate(body) if re.search(r"\bs_(c)?branch\w*\s+" + re.escape(label) + r"\s*$", l)]
-        assert back and all(i > h for i in back), (k, "unexpected loop shape")
-        stores = sum(1 for l in body[tail:h] if re.search(r"\bglobal_store", l))
-        assert stores >= n, (k, stores, n)
-        # nothing on the back-edge path between the last direct load and the header may skip
-        # the tail: the header is entered from the tail (fall through) or from before the loop
-        into_head = [l for l in body if re.search(r"\bs_(c)?branch\w*\s+" + re.escape(body[h].split(":")[0]) + r"\s*$", l)]
-        entry = [i for i, l in enumerate(body) if re.search(r"\bs_(c)?branch\w*\s+" + re.escape(body[h].split(":")[0]) + r"\s*$", l)]
-        assert all(i < tail for i in entry), (k, "header reached around the tail", into_head)
+        head = body[h].split(":")[0]
+        to_head = [i for i, l in enumerate(body) if re.search(r"\bs_(c)?branch\w*\s+" + re.escape(head) + r"\s*$", l)]
+        latch = [i for i in to_head if i > h]
+        last_dma = max(i for i in dma if i < h + 1000)
+        if latch:
+            # the loop is laid out in order: one branch back to the header ends the
+            # iteration, and the block that ends with it (from the last label before
+            # it, which every path of the iteration reaches) holds at least n stores
+            # after the last direct load
+            assert len(latch) == 1, (k, "several back edges")
+            tail = max(i for i in range(latch[0]) if re.match(r"^\.LBB\d+_\d+:", body[i]))
+            assert tail > last_dma, (k, "direct loads after the last join of the iteration")
+            stores = sum(1 for l in body[tail:latch[0]] if re.search(r"\bglobal_store", l))
+            assert stores >= n, (k, stores, n)
+            close = latch[0]
+        else:
+            # the loop is rotated: the block that falls into the header ends the
+            # iteration; every branch back into the loop goes there, and it holds at
+            # least n stores
+            tail = max(i for i in range(h) if re.match(r"^\.LBB\d+_\d+:", body[i]))
+            label = body[tail].split(":")[0]
+            back = [i for i, l in enumerate(body) if re.search(r"\bs_(c)?branch\w*\s+" + re.escape(label) + r"\s*$", l)]
+            assert back and all(i > h for i in back), (k, "unexpected loop shape")
+            stores = sum(1 for l in body[tail:h] if re.search(r"\bglobal_store", l))
+            assert stores >= n, (k, stores, n)
+            # nothing on the back-edge path between the last direct load and the header may
+            # skip the tail: the header is entered from the tail (fall through) or from before
+            # the loop
+            assert all(i < tail for i in to_head), (k, "header reached around the tail")
+            close = max(back)
         # before the loop: the first block's direct loads are followed by a full wait
-        pro = [i for i in range(tail) if "global_load_lds" in body[i]]
+        start = h if latch else tail
+        pro = [i for i in range(start) if "global_load_lds" in body[i]]
         assert pro, (k, "no prologue prefetch")
-        assert any("s_waitcnt vmcnt(0)" in body[i] for i in range(pro[-1], tail)), (k, "prologue not drained")
-        # after the loop (the code after its last branch back into the tail): a full wait
+        assert any("s_waitcnt vmcnt(0)" in body[i] for i in range(pro[-1], start)), (k, "prologue not drained")
+        # after the loop (the code after its last branch back into it): a full wait
         # comes before any LDS instruction and before the end of the program
-        close = max(back)
         rest = body[close + 1:]
         w = next((i for i, l in enumerate(rest) if "s_waitcnt vmcnt(0)" in l), None)
         assert w is not None, (k, "no full wait after the loop")
