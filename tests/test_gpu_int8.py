@@ -221,3 +221,36 @@ def test_many_blocks_per_workgroup(ctx, grid, dtype, k):
         _check(ctx, 7 * 4096 + 100, k, dtype=dtype, seed=50 + grid + k, normalize=grid % 2 == 1)
     finally:
         al.autoloco_set_grid_limit(ctx, 0)
+
+
+@pytest.mark.parametrize("k,dtype", [(4, torch.float32), (8, torch.bfloat16)])
+def test_non_finite_blocks_stay_local(ctx, k, dtype):
+    # a NaN in one block and an infinity in another: the round reports non-finite
+    # statistics, the planted elements come out non-finite, and every other codec
+    # block is exactly what the oracle gives (the codec and the step are local to
+    # a block; inside the planted blocks the paper fixes no NaN arithmetic)
+    n = 6 * 4096 + 1000
+    inp = cpu_inputs(n, k, seed=77, replica_dtype=dtype)
+    nan_at, inf_at = 1 * 4096 + 17, 3 * 4096 + 100
+    inp.replicas[1][nan_at] = float("nan")
+    inp.replicas[k - 1][inf_at] = float("inf")
+    dev = to_device(inp)
+    c = al.make_coeffs(COEFFS["mu"], COEFFS["eta_out"], COEFFS["rho"], True)
+    with np.errstate(all="ignore"):
+        ref = ic.int8_round(inp.theta.numpy(), inp.momentum.numpy(), [host_array(r) for r in inp.replicas],
+                            c.mu, c.eta_out, c.rho, True, EPS)
+    codes, scales = _payload(n)
+    st = al.autoloco_outer_step_int8(ctx, dev.theta, dev.momentum, dev.replicas, c, al.FUSE_STATS | al.FUSE_RESET,
+                                     EPS, mean_codes=codes, mean_scales=scales)
+    torch.cuda.synchronize()
+    assert not st.finite
+    th, v = dev.theta.cpu().numpy(), dev.momentum.cpu().numpy()
+    assert not np.isfinite(th[nan_at]) and not np.isfinite(th[inf_at])
+    keep = [b for b in range((n + 4095) // 4096) if b not in (1, 3)]
+    got_codes, got_scales = codes[:n].cpu().numpy(), scales.cpu().numpy()
+    for b in keep:
+        lo, hi = 4096 * b, min(n, 4096 * (b + 1))
+        assert np.array_equal(got_codes[lo:hi], ref.mean_codes[lo:hi]), b
+        assert got_scales[b].view(np.uint32) == ref.mean_scales[b].view(np.uint32), b
+        assert_close_elementwise(th[lo:hi], ref.theta[lo:hi], what=f"theta' block {b}")
+        assert_close_elementwise(v[lo:hi], ref.momentum[lo:hi], what=f"v' block {b}")
