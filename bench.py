@@ -375,6 +375,38 @@ def bench_inner(args) -> int:
         f"({norm_bytes / norm_mean / 1e6:.0f} GB/s)")
     ceiling = None if args.no_ceiling else copy_ceiling(torch, dev)
     achieved = update_bytes / (upd_mean * 1e-3) / 1e9
+
+    # The update pass's loads and stores without its arithmetic, on the same
+    # buffers and grid; and the norm pass's pattern (K streams read) from the
+    # streaming probe at one, two and three workgroups per compute unit.
+    reference = None
+    if not args.no_ceiling:
+        ref_ms = []
+        for _ in range(10):
+            al.autoloco_adamw_traffic_reference(ctx, st.params, st.exp_avg, st.exp_avg_sq, st.grads,
+                                                model_bf16=copies)
+            ref_ms.append(al.autoloco_last_kernel_ms(ctx))
+        ref_med = statistics.median(ref_ms)
+        reference = {"kernel": "adamw_kernel traffic reference (the update pass's loads and stores, no arithmetic)",
+                     "kernel_ms_median": ref_med, "gbs": update_bytes / (ref_med * 1e-3) / 1e9,
+                     "update_frac_of_reference": ref_med / upd_mean}
+        log(f"update pass traffic reference: {ref_med:.3f} ms ({update_bytes / ref_med / 1e6:.0f} GB/s); the "
+            f"update runs at {100 * ref_med / upd_mean:.1f} % of it")
+        if k in (1, 2, 4, 8, 10):
+            cus = torch.cuda.get_device_properties(0).multi_processor_count
+            best = None
+            for per in (1, 2, 3):
+                pm = []
+                for _ in range(5):
+                    al.autoloco_traffic_probe(ctx, [(g, al.PROBE_READ) for g in st.grads], al.PROBE_RUN1, cus * per)
+                    pm.append(al.autoloco_last_kernel_ms(ctx))
+                m = statistics.median(pm)
+                best = m if best is None else min(best, m)
+            reference["norm_probe_ms"] = best
+            reference["norm_probe_gbs"] = norm_bytes / (best * 1e-3) / 1e9
+            reference["norm_frac_of_probe"] = best / norm_mean
+            log(f"norm pass: probe of {k} streams read {best:.3f} ms ({norm_bytes / best / 1e6:.0f} GB/s); the norm "
+                f"pass runs at {100 * best / norm_mean:.1f} % of it")
     tag = f"adamw_f32_k{k}_{args.workload}" + ("_copy" if args.copy else "")
     traffic = committed_traffic(tag, ADAMW_SOURCES)
 
@@ -418,6 +450,7 @@ def bench_inner(args) -> int:
         "update_ms_mean": upd_mean,
         "norm_ms_mean": norm_mean,
         "norm_pass_gbs": norm_bytes / (norm_mean * 1e-3) / 1e9,
+        "traffic_reference": reference,
         "copy_ceiling_gbs": ceiling,
         "first_step_grad_norms": list(first.grad_norm[:k]) if first is not None else None,
         "cpu_baseline": cpu,

@@ -434,6 +434,16 @@ int autoloco_inner_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* bufs,
  * call (norm_ms = 0 if the norm pass did not run); waits for them to finish. */
 int autoloco_last_adamw_ms(autoloco_ctx* ctx, float* norm_ms, float* update_ms);
 
+/* Measurement, no operation of the paper: the traffic reference of the AdamW
+ * update pass.  It runs that pass's kernel on the same grid with the same
+ * loads and stores and none of the arithmetic: params, exp_avg and exp_avg_sq
+ * keep their bits, grads are read, and each model_bf16 (if set) receives the
+ * BF16 rounding of the unchanged params, which is what the last AdamW step
+ * wrote there.  Asynchronous on the stream; timed like a round
+ * (autoloco_last_kernel_ms).  Errors: as autoloco_inner_adamw's buffer
+ * checks. */
+int autoloco_adamw_traffic_reference(autoloco_ctx* ctx, const autoloco_adamw_buffers* bufs);
+
 /* ------------------------------------------------------------------------ */
 /* Host-only scalar routines                                                 */
 /* ------------------------------------------------------------------------ */

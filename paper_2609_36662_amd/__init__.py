@@ -15,7 +15,7 @@ from ._lib import (  # noqa: F401
     autoloco_lr_mass, autoloco_outer_correction, autoloco_outer_step, autoloco_outer_step_bf16, autoloco_outer_step_int8, autoloco_round_stats,
     autoloco_select_interval, autoloco_set_grid_limit, autoloco_set_timing, default_controller_cfg,
     lib, make_buffers, make_coeffs, make_observation, make_outer_cfg, make_schedule, spread_tensors,
-    autoloco_inner_adamw, autoloco_last_adamw_ms, autoloco_rank_payload, autoloco_shard_step, make_adamw_buffers, make_adamw_coeffs,
+    autoloco_inner_adamw, autoloco_last_adamw_ms, autoloco_adamw_traffic_reference, autoloco_rank_payload, autoloco_shard_step, make_adamw_buffers, make_adamw_coeffs,
     autoloco_traffic_reference, autoloco_traffic_probe, autoloco_build_id, autoloco_outer_step_static,
     PROBE_READ, PROBE_WRITE, PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE,
 )

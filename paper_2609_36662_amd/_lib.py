@@ -158,6 +158,7 @@ SYMBOLS = [
     ("autoloco_inner_adamw", C.c_int, [C.c_void_p, C.POINTER(AdamWBuffers), C.POINTER(AdamWCoeffs),
                                        C.POINTER(AdamWStats)]),
     ("autoloco_last_adamw_ms", C.c_int, [C.c_void_p, C.POINTER(C.c_float), C.POINTER(C.c_float)]),
+    ("autoloco_adamw_traffic_reference", C.c_int, [C.c_void_p, C.POINTER(AdamWBuffers)]),
     ("autoloco_inner_lr", C.c_double, [C.POINTER(Schedule), C.c_int64]),
     ("autoloco_lr_mass", C.c_double, [C.POINTER(Schedule), C.c_int64, C.c_int64]),
     ("autoloco_outer_correction", C.c_int, [C.POINTER(OuterCfg), C.c_double, C.c_double,
@@ -628,6 +629,14 @@ def autoloco_inner_adamw(ctx: Context, params, exp_avg, exp_avg_sq, grads, coeff
     _check(lib().autoloco_inner_adamw(ctx.handle, C.byref(b), C.byref(coeffs),
                                       C.byref(out) if out is not None else None), "autoloco_inner_adamw", ctx)
     return out
+
+
+def autoloco_adamw_traffic_reference(ctx: Context, params, exp_avg, exp_avg_sq, grads, model_bf16=None,
+                                     n=None) -> None:
+    """The AdamW update pass's loads and stores without its arithmetic (a
+    measurement: every buffer keeps what the last step left in it)."""
+    b = make_adamw_buffers(params, exp_avg, exp_avg_sq, grads, model_bf16, n)
+    _check(lib().autoloco_adamw_traffic_reference(ctx.handle, C.byref(b)), "autoloco_adamw_traffic_reference", ctx)
 
 
 def autoloco_last_adamw_ms(ctx: Context):

@@ -24,13 +24,19 @@ hipError_t launch_grad_norm(int k, int blocks, hipStream_t s, const GradNormArgs
     return table[k](blocks, s, a);
 }
 
-hipError_t launch_adamw(bool copy, int k, int blocks_per_worker, hipStream_t s, const AdamWArgs& a) {
+hipError_t launch_adamw(bool copy, bool traffic, int k, int blocks_per_worker, hipStream_t s, const AdamWArgs& a) {
     if (k < 1 || k > kMaxK) return hipErrorInvalidValue;
     const dim3 grid(blocks_per_worker, k);
-    if (copy)
-        hipLaunchKernelGGL(adamw_kernel<true>, grid, dim3(kBlock), 0, s, a);
-    else
-        hipLaunchKernelGGL(adamw_kernel<false>, grid, dim3(kBlock), 0, s, a);
+    if (traffic) {
+        if (copy)
+            hipLaunchKernelGGL((adamw_kernel<true, true>), grid, dim3(kBlock), 0, s, a);
+        else
+            hipLaunchKernelGGL((adamw_kernel<false, true>), grid, dim3(kBlock), 0, s, a);
+    } else if (copy) {
+        hipLaunchKernelGGL((adamw_kernel<true, false>), grid, dim3(kBlock), 0, s, a);
+    } else {
+        hipLaunchKernelGGL((adamw_kernel<false, false>), grid, dim3(kBlock), 0, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -49,6 +49,7 @@ struct AdamWArgs {
     float step_size;         // lr / (1 - beta1^t)
     float inv_sqrt_bc2;      // 1 / sqrt(1 - beta2^t)
     float eps;
+    uint32_t mask;           // traffic reference only: 0 (a value the compiler cannot see)
 };
 
 template <int K>
@@ -97,10 +98,22 @@ __device__ __forceinline__ void adamw_one(const AdamWArgs& a, float coef, float&
 
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 
-template <bool COPY>
+// One element of the traffic reference: the loaded words go back unchanged
+// (a.mask is 0), and the gradient word is folded into the parameter's through
+// the same mask so that its load stays.
+__device__ __forceinline__ void adamw_keep(const AdamWArgs& a, float& p, float& m, float& v, float g) {
+    p = __uint_as_float(__float_as_uint(p) ^ (__float_as_uint(g) & a.mask));
+    m = __uint_as_float(__float_as_uint(m) ^ a.mask);
+    v = __uint_as_float(__float_as_uint(v) ^ a.mask);
+}
+
+// TRAFFIC: the traffic reference of this kernel -- the same grid, loop, loads and
+// stores, none of the arithmetic; θ, m and v keep their bits and the BF16 copy
+// receives the rounding of the unchanged θ (what the last step wrote there).
+template <bool COPY, bool TRAFFIC>
 __global__ void __launch_bounds__(kBlock) adamw_kernel(AdamWArgs a) {
     const int k = blockIdx.y;
-    const float coef = a.norm_sq != nullptr ? clip_coef(a.norm_sq[k], a.max_norm) : 1.0f;
+    const float coef = !TRAFFIC && a.norm_sq != nullptr ? clip_coef(a.norm_sq[k], a.max_norm) : 1.0f;
     float* __restrict__ p = a.params[k];
     float* __restrict__ m = a.exp_avg[k];
     float* __restrict__ v = a.exp_avg_sq[k];
@@ -117,7 +130,10 @@ __global__ void __launch_bounds__(kBlock) adamw_kernel(AdamWArgs a) {
             pe[e] = pv[e];
             me[e] = mv[e];
             ve[e] = vv[e];
-            adamw_one(a, coef, pe[e], me[e], ve[e], gv[e]);
+            if constexpr (TRAFFIC)
+                adamw_keep(a, pe[e], me[e], ve[e], gv[e]);
+            else
+                adamw_one(a, coef, pe[e], me[e], ve[e], gv[e]);
         }
         st_f4(p + 4 * i, f32x4{pe[0], pe[1], pe[2], pe[3]});
         st_f4(m + 4 * i, f32x4{me[0], me[1], me[2], me[3]});
@@ -129,7 +145,10 @@ __global__ void __launch_bounds__(kBlock) adamw_kernel(AdamWArgs a) {
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3)) {
         const int64_t j = nvec * 4 + threadIdx.x;
         float pe = p[j], me = m[j], ve = v[j];
-        adamw_one(a, coef, pe, me, ve, g[j]);
+        if constexpr (TRAFFIC)
+            adamw_keep(a, pe, me, ve, g[j]);
+        else
+            adamw_one(a, coef, pe, me, ve, g[j]);
         p[j] = pe;
         m[j] = me;
         v[j] = ve;
@@ -138,6 +157,6 @@ __global__ void __launch_bounds__(kBlock) adamw_kernel(AdamWArgs a) {
 }
 
 hipError_t launch_grad_norm(int k, int blocks, hipStream_t s, const GradNormArgs& a);
-hipError_t launch_adamw(bool copy, int k, int blocks_per_worker, hipStream_t s, const AdamWArgs& a);
+hipError_t launch_adamw(bool copy, bool traffic, int k, int blocks_per_worker, hipStream_t s, const AdamWArgs& a);
 
 }  // namespace autoloco

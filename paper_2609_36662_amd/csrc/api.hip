@@ -1052,7 +1052,7 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
     a.step_size = static_cast<float>(co->lr / (1.0 - std::pow(co->beta1, t)));
     a.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - std::pow(co->beta2, t)));
     a.eps = static_cast<float>(co->eps);
-    e = launch_adamw(copy, b->k, adamw_blocks(c, b->n, b->k), c->stream, a);
+    e = launch_adamw(copy, false, b->k, adamw_blocks(c, b->n, b->k), c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "AdamW launch");
     if ((ts = timer_stop(c, true, norm_pass)) != AUTOLOCO_OK) return ts;
     if (out != nullptr) {
@@ -1062,6 +1062,33 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
         if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
         finish_adamw(c->host_sums, b->k, co->max_grad_norm, out);
     }
+    c->err.clear();
+    return AUTOLOCO_OK;
+}
+
+int autoloco_adamw_traffic_reference(autoloco_ctx* c, const autoloco_adamw_buffers* b) {
+    bool copy = false;
+    int st = validate_adamw(c, b, &copy);
+    if (st != AUTOLOCO_OK) return st;
+    if (b->n == 0) return AUTOLOCO_OK;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(c, AUTOLOCO_E_DEVICE, "hipSetDevice failed");
+    AdamWArgs a;
+    std::memset(&a, 0, sizeof(a));
+    for (int k = 0; k < b->k; ++k) {
+        a.params[k] = b->params[k];
+        a.exp_avg[k] = b->exp_avg[k];
+        a.exp_avg_sq[k] = b->exp_avg_sq[k];
+        a.grads[k] = b->grads[k];
+        a.copy[k] = static_cast<uint16_t*>(b->model_bf16[k]);
+    }
+    a.n = b->n;
+    a.mask = 0u;
+    int ts = timer_start(c);
+    if (ts != AUTOLOCO_OK) return ts;
+    const hipError_t e = launch_adamw(copy, true, b->k, adamw_blocks(c, b->n, b->k), c->stream, a);
+    if (e != hipSuccess) return hip_fail(c, e, "AdamW traffic reference launch");
+    if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     c->err.clear();
     return AUTOLOCO_OK;
 }

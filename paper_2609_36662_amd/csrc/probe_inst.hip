@@ -20,7 +20,7 @@ struct ProbeEntry {
 // written or not)
 #define AUTOLOCO_PROBE_RUNS(X)                                                                         \
     X(1, 10, 0, 0, 0, 0) X(1, 6, 0, 0, 0, 0) X(1, 4, 0, 0, 0, 0) X(1, 2, 0, 0, 0, 0) X(1, 1, 0, 0, 0, 0) \
-    X(1, 0, 10, 0, 0, 0) X(1, 0, 4, 0, 0, 0) X(1, 0, 2, 0, 0, 0) X(1, 0, 1, 0, 0, 0)                     \
+    X(1, 0, 10, 0, 0, 0) X(1, 0, 8, 0, 0, 0) X(1, 0, 4, 0, 0, 0) X(1, 0, 2, 0, 0, 0) X(1, 0, 1, 0, 0, 0) \
     X(1, 0, 0, 0, 0, 10) X(1, 0, 0, 0, 0, 1) X(1, 0, 5, 0, 0, 5)                                         \
     X(1, 0, 1, 0, 0, 1) X(1, 0, 1, 0, 0, 4) X(1, 0, 1, 0, 0, 8) X(1, 0, 1, 0, 0, 16)                     \
     X(2, 10, 0, 0, 0, 0) X(2, 0, 10, 0, 0, 0)                                                          \

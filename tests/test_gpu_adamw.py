@@ -134,6 +134,31 @@ def test_bf16_copy(ctx):
         assert_bf16_reset_close(bits16(cp[i]), ref.params[i], what=f"bf16 copy {i}")
 
 
+@pytest.mark.parametrize("copy", [False, True])
+def test_traffic_reference_keeps_the_state(ctx, copy):
+    # the update pass's traffic reference (a measurement) leaves every buffer as
+    # the last step left it: state bits unchanged, the BF16 copies rewritten with
+    # the same bits, gradients untouched; bad buffers launch nothing
+    n, k = 3 * 4096 * 64 + 5, 3
+    dev, _, _, cp = _one_step(ctx, n, k, copy=copy, seed=21)
+    torch.cuda.synchronize()
+    before = [t.clone() for t in dev.params + dev.exp_avg + dev.exp_avg_sq + dev.grads + (cp or [])]
+    al.autoloco_adamw_traffic_reference(ctx, dev.params, dev.exp_avg, dev.exp_avg_sq, dev.grads, model_bf16=cp)
+    torch.cuda.synchronize()
+    after = dev.params + dev.exp_avg + dev.exp_avg_sq + dev.grads + (cp or [])
+    for x, y in zip(before, after):
+        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+    f = al.lib().autoloco_adamw_traffic_reference
+    b = al.make_adamw_buffers(dev.params, dev.exp_avg, dev.exp_avg_sq, dev.grads)
+    b.params[1] = dev.params[1].data_ptr() + 4
+    assert f(ctx.handle, C.byref(b)) == -2
+    b.params[1] = dev.exp_avg[0].data_ptr()
+    assert f(ctx.handle, C.byref(b)) == -3
+    torch.cuda.synchronize()
+    assert torch.equal(dev.exp_avg[0].view(torch.int32), before[k].view(torch.int32))
+
+
 def test_no_clipping_asynchronous(ctx):
     cfg = oa.AdamWConfig(max_grad_norm=0.0)
     n, k = 123_457, 4
