@@ -1137,7 +1137,12 @@ def main() -> int:
     # The same round on plain torch allocations (consecutive buffers, adjacent in
     # physical memory), for comparison with the spread placement above.
     plain = None
-    if args.alloc == "spread" and not args.no_plain and args.codec == "fp32":
+    need = n * (8 + k * s_r)
+    free_b = torch.cuda.mem_get_info(dev)[0]
+    if args.alloc == "spread" and not args.no_plain and args.codec == "fp32" and need > free_b - (2 << 30):
+        log(f"plain allocations: skipped ({need / 1e9:.1f} GB more needed, {free_b / 1e9:.1f} GB free)")
+        plain = {"skipped": f"{need / 1e9:.1f} GB needed beside the spread buffers, {free_b / 1e9:.1f} GB free"}
+    elif args.alloc == "spread" and not args.no_plain and args.codec == "fp32":
         alt = drift.empty_inputs(n, k, replica_dtype=tdtype, device=dev)
         drift.fill_theta_momentum(alt, seed=42, recipe=recipe)
         pk, pw = [], []
