@@ -725,7 +725,7 @@ def bench_probe(args) -> int:
     def probe(name, shape, spec, blocks=0):
         streams = [(ts[i], acc) for i, acc in spec]
         moved, med, best = timed(lambda: al.autoloco_traffic_probe(ctx, streams, shape, blocks))
-        row = {"pattern": name, "shape": ["run1", "run2", "serial", "tile"][shape],
+        row = {"pattern": name, "shape": ["run1", "run2", "serial", "tile", "phased"][shape],
                "blocks": blocks or num_cus, "bytes": moved, "ms_median": med, "ms_min": best,
                "gbs": moved / med / 1e6, "frac_of_peak": moved / med / 1e6 / PEAK_HBM_GBS}
         log(f"  {name:52s} {row['shape']:6s} {row['blocks']:5d} wg  {med:8.3f} ms  {row['gbs']:7.0f} GB/s "
@@ -762,7 +762,8 @@ def bench_probe(args) -> int:
             ("10 streams in place, LDS tiles all streams at once", al.PROBE_TILE, [(i, RW) for i in ten]),
             ("10 streams read, LDS tiles stream by stream", al.PROBE_SERIAL, [(i, R) for i in ten]),
             ("10 streams read, LDS tiles all streams at once", al.PROBE_TILE, [(i, R) for i in ten]),
-            ("10 streams written, LDS tiles", al.PROBE_TILE, [(i, W) for i in ten])):
+            ("10 streams written, LDS tiles", al.PROBE_TILE, [(i, W) for i in ten]),
+            ("10 streams in place, grid-wide read and write phases", al.PROBE_PHASED, [(i, RW) for i in ten])):
         rows.append(probe(name, shape, spec, num_cus))
 
     # the fused round and its traffic reference on the same buffers

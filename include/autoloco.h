@@ -305,18 +305,27 @@ int autoloco_traffic_reference(autoloco_ctx* ctx, const autoloco_buffers* bufs);
  *     in LDS with direct loads, stream after stream, at most two streams'
  *     loads in flight, then stores stream by stream) and AUTOLOCO_PROBE_TILE
  *     (the same tiles with all streams' loads in flight at once) 10 streams in
- *     place, read, or written.  Run shapes skip the last n mod 4 elements, tile
- *     shapes the elements past the last whole tile of 4,096.
+ *     place, read, or written; with AUTOLOCO_PROBE_PHASED (read and write
+ *     phases of the whole grid: every workgroup loads a tile of 7,168
+ *     elements of each stream, 3/7 into LDS and 4/7 into registers, then all
+ *     workgroups meet at a grid barrier, store, and meet again; a cooperative
+ *     launch, so blocks may not exceed the workgroups resident at once, one
+ *     per compute unit) 10 streams in place.  Run shapes skip the last n mod 4
+ *     elements, tile shapes the elements past the last whole tile of 4,096,
+ *     the phased shape those past the last whole round of tiles over the grid.
  *   blocks: workgroups (256 threads), 0 = one per compute unit.
  *   *bytes (may be NULL) receives the bytes moved (reads plus writes).
- * Asynchronous on the stream; timed like the other calls.
- * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE. */
+ * Asynchronous on the stream and timed like the other calls, except the phased
+ * shape: it waits for the kernel, whose grid barriers give up (E_STATE) rather
+ * than wait without bound.
+ * Errors: E_INVALID, E_ALIGN, E_ALIAS, E_DEVICE, E_STATE. */
 #define AUTOLOCO_PROBE_READ 1
 #define AUTOLOCO_PROBE_WRITE 2
 #define AUTOLOCO_PROBE_RUN1 0
 #define AUTOLOCO_PROBE_RUN2 1
 #define AUTOLOCO_PROBE_SERIAL 2
 #define AUTOLOCO_PROBE_TILE 3
+#define AUTOLOCO_PROBE_PHASED 4
 typedef struct {
     void* ptr;
     int32_t elem_bytes;

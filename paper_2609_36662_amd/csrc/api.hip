@@ -786,7 +786,7 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
     if (c == nullptr) return AUTOLOCO_E_INVALID;
     if (streams == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null streams");
     if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
-    if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_TILE)
+    if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_PHASED)
         return fail(c, AUTOLOCO_E_INVALID, "unknown probe shape");
     if (count < 1 || count > kProbeMaxStreams) return fail(c, AUTOLOCO_E_INVALID, "stream count outside 1..18");
     if (blocks < 0 || blocks > kMaxBlocks) return fail(c, AUTOLOCO_E_INVALID, "blocks outside 0..16384");
@@ -815,14 +815,20 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
         r.push_back({lo, lo + static_cast<uintptr_t>(n) * static_cast<uintptr_t>(x.elem_bytes), "probe stream"});
     }
     ProbePattern p;
-    p.shape = shape == AUTOLOCO_PROBE_SERIAL ? PROBE_SERIAL : shape == AUTOLOCO_PROBE_TILE ? PROBE_TILE : PROBE_RUN;
+    p.shape = shape == AUTOLOCO_PROBE_SERIAL ? PROBE_SERIAL : shape == AUTOLOCO_PROBE_TILE ? PROBE_TILE
+            : shape == AUTOLOCO_PROBE_PHASED ? PROBE_PHASED : PROBE_RUN;
     p.r = shape == AUTOLOCO_PROBE_RUN2 ? 2 : 1;
     p.a = cls_count[0];
     p.b = cls_count[1];
     p.c = cls_count[2];
     p.d = cls_count[3];
     p.e = cls_count[4];
-    if (!probe_available(p)) return fail(c, AUTOLOCO_E_INVALID, "no probe instance for this pattern and shape");
+    const bool phased = p.shape == PROBE_PHASED;
+    if (phased ? !(p.a == kPhaseStreams && count == kPhaseStreams) : !probe_available(p))
+        return fail(c, AUTOLOCO_E_INVALID, "no probe instance for this pattern and shape");
+    const int nb = blocks > 0 ? blocks : c->num_cus;   // default: one workgroup per compute unit
+    if (phased && nb > probe_phased_occupancy() * c->num_cus)
+        return fail(c, AUTOLOCO_E_INVALID, "phased probe: more workgroups than can be resident at once");
     if (n == 0) {
         if (bytes) *bytes = 0.0;
         return AUTOLOCO_OK;
@@ -837,18 +843,30 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
     a.n = n;
     a.sentinel = 0x9E3779B9u;
     a.sink = reinterpret_cast<uint32_t*>(c->partials);
-    // elements the shape moves per stream: whole runs of 4, or whole tiles
+    // elements the shape moves per stream: whole runs of 4, whole tiles, or
+    // whole rounds of tiles over the grid
     const int64_t tile = 4 * kProbeTileQuads * kBlock;
-    const int64_t moved = p.shape == PROBE_RUN ? n / 4 * 4 : n / tile * tile;
-    const int nb = blocks > 0 ? blocks : c->num_cus;   // default: one workgroup per compute unit
+    const int64_t ptile = 4 * static_cast<int64_t>(kPhaseLdsRuns + kPhaseRegRuns) * kBlock;
+    const int64_t moved = p.shape == PROBE_RUN ? n / 4 * 4 : phased ? n / (ptile * nb) * (ptile * nb) : n / tile * tile;
     double b = 0.0;
     for (int s = 0; s < count; ++s)
         b += static_cast<double>(moved) * streams[s].elem_bytes * (streams[s].access == 3 ? 2 : 1);
+    uint32_t* sync = reinterpret_cast<uint32_t*>(c->partials);   // the phased shape's barrier words
+    hipError_t e;
+    if (phased && (e = hipMemsetAsync(sync, 0, 2 * sizeof(uint32_t), c->stream)) != hipSuccess)
+        return hip_fail(c, e, "hipMemsetAsync");
     int ts = timer_start(c);
     if (ts != AUTOLOCO_OK) return ts;
-    const hipError_t e = launch_probe(p, nb, c->stream, a);
+    e = phased ? launch_probe_phased(nb, c->stream, a, sync) : launch_probe(p, nb, c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
     if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
+    if (phased) {
+        uint32_t words[2] = {0, 0};
+        if ((e = hipMemcpyAsync(words, sync, sizeof(words), hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
+            return hip_fail(c, e, "hipMemcpyAsync");
+        if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        if (words[1] != 0) return fail(c, AUTOLOCO_E_STATE, "phased probe: a grid barrier gave up waiting");
+    }
     if (bytes) *bytes = b;
     c->err.clear();
     return AUTOLOCO_OK;

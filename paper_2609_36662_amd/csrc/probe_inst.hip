@@ -53,6 +53,21 @@ bool probe_available(const ProbePattern& p) {
     return false;
 }
 
+hipError_t launch_probe_phased(int blocks, hipStream_t stream, const ProbeArgs& a, uint32_t* sync) {
+    ProbeArgs args = a;
+    uint32_t* sy = sync;
+    void* params[] = {&args, &sy};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(probe_phase_kernel<kPhaseStreams>), dim3(blocks),
+                                      dim3(kBlock), params, 0, stream);
+}
+
+int probe_phased_occupancy() {
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, probe_phase_kernel<kPhaseStreams>, kBlock, 0) != hipSuccess)
+        return 0;
+    return b;
+}
+
 hipError_t launch_probe(const ProbePattern& p, int blocks, hipStream_t s, const ProbeArgs& a) {
     for (const ProbeEntry& e : kProbes) {
         if (!same(e.p, p)) continue;

@@ -27,7 +27,14 @@
 //            workgroup at most), then stores the tile stream by stream;
 //   tile     the same tiles with every stream's loads issued at once, waited
 //            for together, then stored: read and write phases of up to 160 KB
-//            per workgroup.
+//            per workgroup;
+//   phased   read and write phases of the whole grid: every workgroup loads
+//            its tile of every stream (3 runs of 4 per lane into LDS with
+//            direct loads, 4 more into registers: 280 KB per workgroup over ten
+//            streams), waits for them, meets every other workgroup at a grid
+//            barrier, stores the tile, waits, and meets them again, so the
+//            device reads and writes in alternating phases of about 70 MB
+//            (cooperative launch, one workgroup per compute unit).
 // Run shapes skip the last n mod 4 elements, tile shapes the elements past the
 // last whole tile (4 runs of 4 per lane: 4,096 elements).
 #pragma once
@@ -44,7 +51,7 @@ constexpr int kProbeTileStreams = 10;         // the tile shapes' LDS holds this
 constexpr int kProbeTileQuads = 4;            // runs of 4 per lane per stream per tile
 constexpr int kProbePieces = 40;              // LDS pieces of 4 KB (one run per lane of a workgroup)
 
-enum ProbeShape { PROBE_RUN = 0, PROBE_SERIAL = 1, PROBE_TILE = 2 };
+enum ProbeShape { PROBE_RUN = 0, PROBE_SERIAL = 1, PROBE_TILE = 2, PROBE_PHASED = 3 };
 
 struct ProbeArgs {
     void* ptr[kProbeMaxStreams];
@@ -182,6 +189,103 @@ __global__ void __launch_bounds__(kBlock) probe_tile_kernel(ProbeArgs a) {
     AUTOLOCO_WAIT_VMCNT(0);
     if (fold == a.sentinel) a.sink[blockIdx.x] = fold;
 }
+
+// Phased shape: runs of 4 per lane per stream per tile held in LDS and in
+// registers, and the polls after which a grid barrier gives up.
+constexpr int kPhaseLdsRuns = 3;
+constexpr int kPhaseRegRuns = 4;
+constexpr int kPhaseStreams = 10;
+constexpr uint32_t kPhaseSpin = 1u << 22;
+
+// Grid barrier of a cooperative launch (every workgroup resident at once).
+// sync[0] counts arrivals over the whole launch (target: the barrier's number
+// times the grid), sync[1] is set by a workgroup that gave up.  Thread 0 adds
+// its arrival and polls, sleeping between polls; after kPhaseSpin polls, or as
+// soon as another workgroup has given up, it sets sync[1] and reports failure,
+// and every workgroup then leaves its loop, so the grid always drains.  The
+// decision reaches the workgroup's other threads through LDS, so they all take
+// the same branch.  Vector memory atomics only.
+__device__ __forceinline__ bool phase_barrier(uint32_t* sync, uint32_t target, uint32_t* ok) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t good = 1;
+        __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (uint32_t i = 0; __hip_atomic_load(sync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target; ++i) {
+            if (i >= kPhaseSpin || __hip_atomic_load(sync + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                __hip_atomic_store(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                good = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+        }
+        *ok = good;
+    }
+    __syncthreads();
+    return *ok != 0;
+}
+
+// Phased shape, A 4-byte streams read and written back in place.  Tile t
+// (workgroup b's in round r: t = r * grid + b) covers 7 * 256 quads of every
+// stream; run u of lane i is quad u * 256 + i.  Only whole rounds of tiles over
+// the grid are moved (every workgroup meets every barrier).
+template <int A>
+__global__ void __launch_bounds__(kBlock, 1) probe_phase_kernel(ProbeArgs a, uint32_t* sync) {
+    constexpr int UL = kPhaseLdsRuns, UR = kPhaseRegRuns, U = UL + UR;
+    __shared__ u32x4 lds[A * UL * kBlock];
+    __shared__ uint32_t ok;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    constexpr int64_t tq = (int64_t)U * kBlock;
+    const int64_t rounds = a.n / 4 / tq / gridDim.x;
+    uint32_t target = 0;
+    for (int64_t r = 0; r < rounds; ++r) {
+        const int64_t w0 = (r * gridDim.x + blockIdx.x) * tq * 4;
+        u32x4 x[A][UR];
+#pragma unroll
+        for (int s = 0; s < A; ++s) {
+#pragma unroll
+            for (int u = 0; u < UL; ++u) {
+                const uint32_t* src = static_cast<const uint32_t*>(a.ptr[s]) + w0 + (int64_t)(u * kBlock + threadIdx.x) * 4;
+                __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                                 (void __attribute__((address_space(3)))*)(lds + (s * UL + u) * kBlock + wave * 64),
+                                                 16, 0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < UR; ++u)
+                x[s][u] = ld_u4_at(static_cast<const uint32_t*>(a.ptr[s]) + w0, (uint32_t)((UL + u) * kBlock + threadIdx.x) * 16u);
+        }
+        // the read phase ends when this workgroup's loads have all landed
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        target += gridDim.x;
+        if (!phase_barrier(sync, target, &ok)) break;
+#pragma unroll
+        for (int s = 0; s < A; ++s) {
+#pragma unroll
+            for (int u = 0; u < UL; ++u)
+                st_u4_at(static_cast<uint32_t*>(a.ptr[s]) + w0, (uint32_t)(u * kBlock + threadIdx.x) * 16u,
+                         lds[(s * UL + u) * kBlock + wave * 64 + lane] ^ a.mask);
+#pragma unroll
+            for (int u = 0; u < UR; ++u)
+                st_u4_at(static_cast<uint32_t*>(a.ptr[s]) + w0, (uint32_t)((UL + u) * kBlock + threadIdx.x) * 16u,
+                         x[s][u] ^ a.mask);
+        }
+        // the write phase ends when the stores are done (and the LDS reads have
+        // returned, before the next round's direct loads reuse the pieces)
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        target += gridDim.x;
+        if (!phase_barrier(sync, target, &ok)) break;
+    }
+}
+
+// Launches the phased probe over kPhaseStreams streams in place as a
+// cooperative launch; sync: two zeroed words (see phase_barrier).
+hipError_t launch_probe_phased(int blocks, hipStream_t stream, const ProbeArgs& a, uint32_t* sync);
+// Workgroups of the phased probe that fit on one compute unit.
+int probe_phased_occupancy();
 
 // One instantiated pattern: shape, runs per lane (run shape), class counts.
 struct ProbePattern {

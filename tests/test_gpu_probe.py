@@ -134,3 +134,30 @@ def test_bad_arguments_launch_nothing(ctx):
     torch.cuda.synchronize()
     for i, b in enumerate(bufs + half):
         assert np.array_equal(_bits(b), before[i])
+
+
+PHASE_TILE = 7 * 4 * 256      # elements of one phased tile per stream
+
+
+@pytest.mark.parametrize("blocks", [1, 3, 0])
+def test_phased_keeps_bits_and_counts_whole_rounds(ctx, blocks):
+    grid = blocks or torch.cuda.get_device_properties(0).multi_processor_count
+    n = 2 * grid * PHASE_TILE + 1000 if blocks else grid * PHASE_TILE + 77
+    bufs = _bufs(n, 10, seed=blocks + 40)
+    before = [_bits(b) for b in bufs]
+    moved = al.autoloco_traffic_probe(ctx, [(b, RW) for b in bufs], al.PROBE_PHASED, blocks)
+    torch.cuda.synchronize()
+    for i, b in enumerate(bufs):
+        assert np.array_equal(_bits(b), before[i]), f"stream {i} changed"
+    assert moved == 4.0 * (n // (grid * PHASE_TILE)) * grid * PHASE_TILE * 10 * 2
+
+
+def test_phased_rejects_other_patterns(ctx):
+    bufs = _bufs(PHASE_TILE, 10, seed=9)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for spec, blocks in (([(b, RW) for b in bufs[:9]], 1),          # nine streams
+                         ([(b, R) for b in bufs], 1),               # read only
+                         ([(b, RW) for b in bufs], 2 * cus + 1)):   # more workgroups than fit at once
+        with pytest.raises(al.AutolocoError) as e:
+            al.autoloco_traffic_probe(ctx, spec, al.PROBE_PHASED, blocks)
+        assert e.value.status == -1
