@@ -262,7 +262,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
     // the sets swap roles (current / next) instead of being copied
     u32x2 wA[KW][G], wB[PF ? KW : 1][G];
     float tA[V], tB[PF ? V : 1];
-    float mA[PF || LP ? V : 1], mB[PF ? V : 1];
+    float mA[PF ? V : 1], mB[PF ? V : 1];
     auto load_bf16 = [&](int64_t b, auto& w, float (&t)[V], auto& m, auto full_c) {
         constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
@@ -355,29 +355,20 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
                 // outstanding" imply the loads have landed in LDS.
                 constexpr int after = G * (2 + (RESET ? K : 0));
                 __builtin_amdgcn_s_waitcnt((after & 0xF) | ((after >> 4) << 14) | 0x70 | 0xF00);
-                // momentum: this block's was loaded in the previous iteration; the
-                // next block's is loaded now, ahead of the direct loads below (so
-                // the count above never includes it, wherever the compiler puts it)
-#pragma unroll
-                for (int e = 0; e < V; ++e) v[e] = cm[e];
-                const int64_t nb = blk + gridDim.x < nfull ? blk + gridDim.x : blk;
-#pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const f32x4 m4 = ld_f4(a.momentum + nb * kCodecBlock + g * (kCodecBlock / 2) + (int64_t)threadIdx.x * W);
-#pragma unroll
-                    for (int e = 0; e < W; ++e) cm[g * W + e] = m4[e];
-                }
             }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const int64_t o = off[g];
                 if constexpr (FULL && LP) {
                     // theta and the replicas from the LDS prefetch (complete: see the
-                    // wait above)
+                    // wait above), momentum from memory
                     const int lane = threadIdx.x & 63;
-                    const f32x4 t4 = pf_piece(0, g)[lane];
+                    const f32x4 t4 = pf_piece(0, g)[lane], v4 = ld_f4(a.momentum + o);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) th[g * W + e] = t4[e];
+                    for (int e = 0; e < 4; ++e) {
+                        th[g * W + e] = t4[e];
+                        v[g * W + e] = v4[e];
+                    }
 #pragma unroll
                     for (int k = 0; k < K; ++k) {
                         const f32x4 r4 = pf_piece(k + 1, g)[lane];
@@ -608,16 +599,7 @@ __global__ void __launch_bounds__(kInt8Threads) int8_round_kernel(Int8Args a) {
         }
     } else {
         if constexpr (LP) {
-            if (blockIdx.x < nfull) {
-#pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const f32x4 m4 = ld_f4(a.momentum + (int64_t)blockIdx.x * kCodecBlock + g * (kCodecBlock / 2) +
-                                           (int64_t)threadIdx.x * W);
-#pragma unroll
-                    for (int e = 0; e < W; ++e) mA[g * W + e] = m4[e];
-                }
-                pf_issue(blockIdx.x);
-            }
+            if (blockIdx.x < nfull) pf_issue(blockIdx.x);
             __builtin_amdgcn_s_waitcnt(0);   // the first block's pieces are in LDS
         }
         for (int64_t blk = blockIdx.x; blk < nfull; blk += gridDim.x) body(blk, BoolC<true>{}, wA, tA, mA, wB, tB, mB);
