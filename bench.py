@@ -301,6 +301,98 @@ def inner_cpu_baseline(sample, lr, step, seconds: float, desc: str, threads: int
                       f"norm), step repeated {done // (n * k)}x over {dt:.1f} s (numpy float64, {how})"}
 
 
+# A worker process's view of the inner step's shared chunk buffers: (theta, m, v, g).
+_INNER = None
+
+
+def _attach_inner(names, c):
+    """Worker initialiser: map the inner step's shared chunk buffers (numpy views)."""
+    import numpy as np
+    from multiprocessing import shared_memory
+    global _INNER
+    shms = [shared_memory.SharedMemory(name=x) for x in names]
+    _INNER = [np.ndarray((c,), dtype=np.float32, buffer=m.buf) for m in shms] + [shms]
+
+
+def _inner_norm_part(job):
+    """The oracle's gradient norm of [lo, hi) of the shared chunk, squared."""
+    from oracle import adamw as oa
+    lo, hi = job
+    return oa.grad_norm(_INNER[3][lo:hi]) ** 2
+
+
+def _inner_update_part(job):
+    """The oracle's AdamW step on [lo, hi) of the shared chunk (results dropped)."""
+    from oracle import adamw as oa
+    lo, hi, lr, step, coef = job
+    th, m, v, g = _INNER[:4]
+    oa.adamw_step(th[lo:hi], m[lo:hi], v[lo:hi], g[lo:hi], lr, step, oa.AdamWConfig(), coef)
+    return None
+
+
+def make_inner_pool(n, procs):
+    """Shared chunk buffers (theta, m, v, g) and a pool of worker processes started
+    fresh (spawn), before this process touches the GPU; returns (pool, buffers)."""
+    import multiprocessing as mp
+    from multiprocessing import shared_memory
+    c = min(n, CPU_CHUNK)
+    shms = [shared_memory.SharedMemory(create=True, size=c * 4) for _ in range(4)]
+    names = [m.name for m in shms]
+    pool = mp.get_context("spawn").Pool(procs, initializer=_attach_inner, initargs=(names, c))
+    _attach_inner(names, c)
+    return pool, shms
+
+
+def inner_cpu_baseline_stream(st, lr, step, desc, pool_shms, procs):
+    """The float64 oracle's inner step, as it stands, over the whole workload:
+    for each worker, its gradient's norm (chunk by chunk, the parts' squares
+    added in chunk order) and clipping factor, then its AdamW step.  The buffers
+    move device-to-host in chunks of 2^24 parameters into shared memory (not
+    timed); each chunk's oracle work is split over `procs` worker processes, and
+    only that compute is timed.  Returns the leg and the oracle's norms."""
+    import math
+    from oracle import adamw as oa
+    pool, _ = pool_shms
+    th_s, m_s, v_s, g_s = _INNER[:4]
+    n, k = st.params[0].numel(), len(st.params)
+    cfg = oa.AdamWConfig()
+    t_par, norms, done = 0.0, [], 0
+
+    def jobs(m):
+        step_ = -(-m // procs)
+        return [(lo, min(m, lo + step_)) for lo in range(0, m, step_)]
+
+    for w in range(k):
+        sq = 0.0
+        for c0 in range(0, n, CPU_CHUNK):
+            c1 = min(n, c0 + CPU_CHUNK)
+            g_s[:c1 - c0] = st.grads[w][c0:c1].cpu().numpy()
+            t0 = time.perf_counter()
+            parts = pool.map(_inner_norm_part, jobs(c1 - c0))
+            t_par += time.perf_counter() - t0
+            for x in parts:
+                sq += x
+        norm = math.sqrt(sq)
+        coef = oa.clip_coefficient(norm, cfg.max_grad_norm)
+        norms.append(norm)
+        for c0 in range(0, n, CPU_CHUNK):
+            c1 = min(n, c0 + CPU_CHUNK)
+            for dst, src in ((th_s, st.params[w]), (m_s, st.exp_avg[w]), (v_s, st.exp_avg_sq[w]), (g_s, st.grads[w])):
+                dst[:c1 - c0] = src[c0:c1].cpu().numpy()
+            t0 = time.perf_counter()
+            pool.map(_inner_update_part, [(lo, hi, lr, step, coef) for lo, hi in jobs(c1 - c0)])
+            t_par += time.perf_counter() - t0
+        done += n
+        log(f"oracle: worker {w + 1} of {k} done, {t_par:.1f} s of oracle time so far")
+    nchunks = -(-n // CPU_CHUNK)
+    leg = {"value": n * k / t_par, "unit": "worker-params/s", "cores": procs, "kind": "oracle",
+           "sample": f"{desc}: the whole workload, {n:,} parameters of each of {k} workers, streamed "
+                     f"device-to-host in {nchunks} chunks of up to {CPU_CHUNK:,} per buffer (transfer not timed); "
+                     f"numpy float64 oracle (gradient norm, clipping, AdamW step), each chunk split over "
+                     f"{procs} worker processes", "seconds": t_par}
+    return leg, norms
+
+
 def bench_inner(args) -> int:
     """One AdamW step of every worker (gradient-norm pass + update pass) per timed step."""
     import torch
@@ -313,6 +405,11 @@ def bench_inner(args) -> int:
     n = (1 << 20) if shape_name is None else shapes.SHAPES[shape_name]().n_params
     update_bytes = n * k * (28 + (2 if args.copy else 0))
     norm_bytes = n * k * 4
+    # the CPU baseline's worker processes start before this process touches the GPU
+    pool = procs = None
+    if not args.no_cpu_baseline:
+        procs = cpu_procs(args.cpu_procs)
+        pool = make_inner_pool(n, procs)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     sched = al.make_schedule()
@@ -413,13 +510,16 @@ def bench_inner(args) -> int:
     cpu = cpu1 = None
     if sample is not None:
         desc = f"{args.workload} K={k} inner AdamW"
-        p = host_threads()
         lr = al.autoloco_inner_lr(sched, s0)
-        log(f"timing the oracle on the CPU sample: one thread, then {min(p, k)} threads")
+        log("timing the oracle on the CPU sample on one thread")
         cpu1 = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc)
-        cpu = inner_cpu_baseline(sample, lr, 1000, args.cpu_seconds, desc, threads=min(p, k)) \
-            if min(p, k) > 1 else cpu1
-        for leg in {id(cpu): cpu, id(cpu1): cpu1}.values():
+        log(f"timing the oracle over the whole workload on {procs} processes")
+        cpu, onorms = inner_cpu_baseline_stream(st, lr, 1000, desc, pool, procs)
+        gnorms = list(first.grad_norm[:k]) if first is not None else []
+        match = len(gnorms) == k and all(abs(a - b) <= 1e-6 * abs(b) for a, b in zip(gnorms, onorms))
+        log(f"oracle gradient norms over the whole workload {'within' if match else 'OUTSIDE'} 1e-6 of the GPU's")
+        cpu["grad_norms_match_gpu_within_1e-6"] = match
+        for leg in (cpu, cpu1):
             leg["cpu_model"] = cpu_model()
             leg["gpu_speedup"] = (n * k / (ms_per_step * 1e-3)) / leg["value"]
 
@@ -458,6 +558,7 @@ def bench_inner(args) -> int:
         "kernel_source_sha256_16": kernel_source_hash(ADAMW_SOURCES),
     }
     print(json.dumps(out), flush=True)
+    close_cpu_pool(pool)
     del st, copies, ts
     ctx.close()
     return 0

@@ -68,3 +68,29 @@ def test_streamed_cpu_baseline_equals_one_oracle_pass():
             assert none is None and par2["cores"] == 2 and (st2.D, st2.C) == (st.D, st.C)
     finally:
         bench.CPU_CHUNK = old
+
+
+def test_streamed_inner_cpu_baseline_gives_the_oracle_norms():
+    # the inner step's chunked, multi-process oracle pass computes each worker's
+    # gradient norm over the whole gradient (float64, chunk order)
+    import math
+    sys.path.insert(0, ROOT)
+    import bench
+    from oracle import adamw as oa
+    from workloads import inner
+    old = bench.CPU_CHUNK
+    bench.CPU_CHUNK = 1 << 14
+    try:
+        n, k = 2 * (1 << 14) + 21, 3
+        st = inner.make_state(n, k, seed=9)
+        pool = bench.make_inner_pool(n, 2)
+        try:
+            leg, norms = bench.inner_cpu_baseline_stream(st, 3e-4, 5, "check", pool, 2)
+        finally:
+            bench.close_cpu_pool(pool)
+        for w in range(k):
+            ref = oa.grad_norm(st.grads[w].numpy())
+            assert math.isclose(norms[w], ref, rel_tol=1e-12)
+        assert leg["cores"] == 2 and "3 chunks" in leg["sample"] and leg["value"] > 0
+    finally:
+        bench.CPU_CHUNK = old
