@@ -75,7 +75,8 @@ const char* autoloco_status_string(int status);
 
 /* A context binds one device and one HIP stream and owns the scratch memory of
  * the two-stage statistics reduction (per-block fp64 partial sums and the
- * final sums) plus a pinned host buffer for them.  One context
+ * final sums) plus a pinned, coherent host buffer that the reduction writes
+ * them to.  One context
  * serves one stream; calls on one context must not overlap.
  *   device: HIP device ordinal.  stream: a hipStream_t of that device, or NULL
  *   for the default stream.  *out receives the context.

@@ -55,6 +55,7 @@ struct autoloco_ctx {
     double* partials = nullptr;
     double* sums = nullptr;
     double* host_sums = nullptr;
+    double* host_sums_dev = nullptr;  // device view of host_sums (coherent host memory), or null
     bool timing = false;
     bool timed_valid = false;
     hipEvent_t ev_start = nullptr, ev_stop = nullptr, ev_mid = nullptr;
@@ -261,6 +262,19 @@ int timer_stop(autoloco_ctx* c, bool adamw = false, bool norm_ran = false) {
     return AUTOLOCO_OK;
 }
 
+// Brings the count sums of the last reduction to host_sums and waits for them:
+// with a device view of host_sums the reduction kernel already wrote them there
+// (coherent host memory, visible once the stream has finished), else a copy.
+int sums_to_host(autoloco_ctx* c, size_t count) {
+    hipError_t e;
+    if (c->host_sums_dev == nullptr &&
+        (e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double) * count, hipMemcpyDeviceToHost, c->stream)) !=
+            hipSuccess)
+        return hip_fail(c, e, "hipMemcpyAsync");
+    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+    return AUTOLOCO_OK;
+}
+
 // Launches one round kernel (timed if requested); with stats, waits for the
 // sums and fills *out.
 int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, int mode, bool stats,
@@ -270,16 +284,12 @@ int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, 
     if (ts != AUTOLOCO_OK) return ts;
     hipError_t e = launcher(b->replica_dtype, mode)(b->k, blocks, ctx->stream, a);
     if (e != hipSuccess) return hip_fail(ctx, e, "kernel launch");
-    if (stats && (e = launch_finish_sums(2 * b->k + 1, kBlock, blocks, ctx->partials, ctx->sums, ctx->stream)) !=
-                     hipSuccess)
+    if (stats && (e = launch_finish_sums(2 * b->k + 1, kBlock, blocks, ctx->partials, ctx->sums, ctx->stream,
+                                         ctx->host_sums_dev)) != hipSuccess)
         return hip_fail(ctx, e, "reduction launch");
     if ((ts = timer_stop(ctx)) != AUTOLOCO_OK) return ts;
     if (stats) {
-        const size_t bytes = sizeof(double) * (2 * b->k + 1);
-        e = hipMemcpyAsync(ctx->host_sums, ctx->sums, bytes, hipMemcpyDeviceToHost, ctx->stream);
-        if (e != hipSuccess) return hip_fail(ctx, e, "hipMemcpyAsync");
-        e = hipStreamSynchronize(ctx->stream);
-        if (e != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+        if ((ts = sums_to_host(ctx, 2 * b->k + 1)) != AUTOLOCO_OK) return ts;
         finish_stats(ctx->host_sums, b->k, eps, out);
     }
     ctx->err.clear();
@@ -368,13 +378,11 @@ int run_one_sum(autoloco_ctx* c, Launch launch, int blocks, double* out) {
     if (ts != AUTOLOCO_OK) return ts;
     hipError_t e;
     if ((e = launch()) != hipSuccess) return hip_fail(c, e, "kernel launch");
-    if ((e = launch_finish_sums(1, kBlock, blocks, c->partials, c->sums, c->stream)) != hipSuccess)
+    if ((e = launch_finish_sums(1, kBlock, blocks, c->partials, c->sums, c->stream, c->host_sums_dev)) != hipSuccess)
         return hip_fail(c, e, "reduction launch");
     if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     if (out != nullptr) {
-        if ((e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double), hipMemcpyDeviceToHost, c->stream)) != hipSuccess)
-            return hip_fail(c, e, "hipMemcpyAsync");
-        if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        if ((ts = sums_to_host(c, 1)) != AUTOLOCO_OK) return ts;
         *out = c->host_sums[0];
     }
     c->err.clear();
@@ -535,7 +543,9 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
     }
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
               hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
-              hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocDefault) == hipSuccess;
+              hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocMapped | hipHostMallocCoherent) ==
+                  hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_sums_dev), c->host_sums, 0) == hipSuccess;
     ok = ok && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
     ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess &&
          hipEventCreate(&c->ev_mid) == hipSuccess;
@@ -731,16 +741,12 @@ int autoloco_outer_step_int8(autoloco_ctx* c, const autoloco_buffers* b, const a
     if (ts != AUTOLOCO_OK) return ts;
     hipError_t e = table[rt][stats ? 1 : 0][reset ? 1 : 0](b->k, blocks, c->stream, a);
     if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
-    if (stats && (e = launch_finish_sums(2 * b->k + 1, kInt8Threads, blocks, c->partials, c->sums, c->stream)) !=
-                     hipSuccess)
+    if (stats && (e = launch_finish_sums(2 * b->k + 1, kInt8Threads, blocks, c->partials, c->sums, c->stream,
+                                         c->host_sums_dev)) != hipSuccess)
         return hip_fail(c, e, "reduction launch");
     if ((ts = timer_stop(c)) != AUTOLOCO_OK) return ts;
     if (stats) {
-        const size_t bytes = sizeof(double) * (2 * b->k + 1);
-        e = hipMemcpyAsync(c->host_sums, c->sums, bytes, hipMemcpyDeviceToHost, c->stream);
-        if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync");
-        e = hipStreamSynchronize(c->stream);
-        if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        if ((ts = sums_to_host(c, 2 * b->k + 1)) != AUTOLOCO_OK) return ts;
         finish_stats(c->host_sums, b->k, eps, out);
     }
     c->err.clear();
@@ -1045,7 +1051,7 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
         const int nblocks = blocks_for(c, b->n, AUTOLOCO_F32, b->k, false, false);
         e = launch_grad_norm(b->k, nblocks, c->stream, na);
         if (e != hipSuccess) return hip_fail(c, e, "gradient norm launch");
-        e = launch_finish_sums(b->k, kBlock, nblocks, c->partials, c->sums, c->stream);
+        e = launch_finish_sums(b->k, kBlock, nblocks, c->partials, c->sums, c->stream, c->host_sums_dev);
         if (e != hipSuccess) return hip_fail(c, e, "reduction launch");
     }
     if (c->timing && (e = hipEventRecord(c->ev_mid, c->stream)) != hipSuccess) return hip_fail(c, e, "hipEventRecord");
@@ -1074,10 +1080,7 @@ int autoloco_inner_adamw(autoloco_ctx* c, const autoloco_adamw_buffers* b, const
     if (e != hipSuccess) return hip_fail(c, e, "AdamW launch");
     if ((ts = timer_stop(c, true, norm_pass)) != AUTOLOCO_OK) return ts;
     if (out != nullptr) {
-        e = hipMemcpyAsync(c->host_sums, c->sums, sizeof(double) * b->k, hipMemcpyDeviceToHost, c->stream);
-        if (e != hipSuccess) return hip_fail(c, e, "hipMemcpyAsync");
-        e = hipStreamSynchronize(c->stream);
-        if (e != hipSuccess) return hip_fail(c, e, "hipStreamSynchronize");
+        if ((ts = sums_to_host(c, b->k)) != AUTOLOCO_OK) return ts;
         finish_adamw(c->host_sums, b->k, co->max_grad_norm, out);
     }
     c->err.clear();

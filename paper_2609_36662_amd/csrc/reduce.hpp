@@ -57,7 +57,8 @@ __device__ __forceinline__ void store_partials(double (&acc)[NS], double* partia
 // thread t adds the partials of workgroups t, t + NT, ... in that order, then
 // the workgroup reduces those as in stage 1; sums[0..NS) receives the totals.
 template <int NS, int NT>
-__global__ void __launch_bounds__(NT) finish_sums_kernel(const double* partials, int nblocks, double* sums) {
+__global__ void __launch_bounds__(NT) finish_sums_kernel(const double* partials, int nblocks, double* sums,
+                                                         double* host_copy) {
     __shared__ double lds[kMaxWaves * kMaxSums];
     double tot[NS];
 #pragma unroll
@@ -67,11 +68,16 @@ __global__ void __launch_bounds__(NT) finish_sums_kernel(const double* partials,
         for (int j = 0; j < NS; ++j) tot[j] += partials[(int64_t)b * NS + j];
     }
     const double fin = block_reduce<NS, NT>(tot, lds);
-    if (threadIdx.x < NS) sums[threadIdx.x] = fin;
+    if (threadIdx.x < NS) {
+        sums[threadIdx.x] = fin;
+        if (host_copy != nullptr) host_copy[threadIdx.x] = fin;
+    }
 }
 
-// Launches finish_sums_kernel for ns in 1..kMaxSums and nt in {256, 512}.
+// Launches finish_sums_kernel for ns in 1..kMaxSums and nt in {256, 512};
+// host_copy (may be null): a device view of coherent host memory that receives
+// the sums as well, so no copy is needed to bring them to the host.
 hipError_t launch_finish_sums(int ns, int nt, int nblocks, const double* partials, double* sums,
-                              hipStream_t stream);
+                              hipStream_t stream, double* host_copy = nullptr);
 
 }  // namespace autoloco
