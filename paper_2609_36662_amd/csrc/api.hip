@@ -544,8 +544,13 @@ int autoloco_create(int device, void* stream, autoloco_ctx** out) {
     bool ok = hipMalloc(&c->partials, sizeof(double) * kMaxSums * kMaxBlocks) == hipSuccess &&
               hipMalloc(&c->sums, sizeof(double) * kMaxSums) == hipSuccess &&
               hipHostMalloc(&c->host_sums, sizeof(double) * kMaxSums, hipHostMallocMapped | hipHostMallocCoherent) ==
-                  hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_sums_dev), c->host_sums, 0) == hipSuccess;
+                  hipSuccess;
+    // the reduction writes the sums to host_sums through its device view; without
+    // one, they are copied
+    if (ok && hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_sums_dev), c->host_sums, 0) != hipSuccess) {
+        c->host_sums_dev = nullptr;
+        (void)hipGetLastError();
+    }
     ok = ok && hipMemset(c->sums, 0, sizeof(double) * kMaxSums) == hipSuccess;
     ok = ok && hipEventCreate(&c->ev_start) == hipSuccess && hipEventCreate(&c->ev_stop) == hipSuccess &&
          hipEventCreate(&c->ev_mid) == hipSuccess;
