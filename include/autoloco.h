@@ -100,7 +100,7 @@ int autoloco_set_timing(autoloco_ctx* ctx, int enable);
 int autoloco_last_kernel_ms(autoloco_ctx* ctx, float* ms);
 /* Cap on the number of workgroups of the streaming kernels, 0..16384 (0 = the
  * default: one workgroup per compute unit from k = 5 with fp32 replicas and
- * from k = 8 with bf16, below that three, or fewer
+ * from k = 6 with bf16, below that three, or fewer
  * if the fused kernel's register use fits fewer).  The statistics
  * are bit-identical between runs with the same n, k, replica type, device and
  * cap, and between the standalone and the fused call. */

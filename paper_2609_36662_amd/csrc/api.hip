@@ -32,7 +32,7 @@ namespace {
 constexpr int kMaxBlocks = 16384;   // scratch sized for this many workgroups
 
 // Workgroups whose partial sums the static scratch below holds: the default
-// grid is one workgroup per compute unit from K = 5 (fp32 replicas) or 8 (bf16)
+// grid is one workgroup per compute unit from K = 5 (fp32 replicas) or 6 (bf16)
 // and three below (768 on MI355X).
 constexpr int kStaticBlocks = 1024;
 
@@ -108,14 +108,14 @@ int check_device_ptr(autoloco_ctx* ctx, uintptr_t p, const char* name) {
     return AUTOLOCO_OK;
 }
 
-// Default grid: from K = 5 with fp32 replicas and from K = 8 with bf16 one
+// Default grid: from K = 5 with fp32 replicas and from K = 6 with bf16 one
 // workgroup per compute unit (4 waves), below that three, or fewer if fewer fit
 // (the fused kernel's occupancy).  Measured on MI355X (256 CUs) with the
 // round's buffers spread in HBM, 1.1B K = 8 fp32: fused round 14.14-14.27 ms at
 // 256 workgroups against 14.37-14.57 at 768 (the traffic reference alike), and
 // no mode slower (statistics only 6.28 against 6.37 ms, with its windows loaded
-// ahead); 3B K = 8 bf16, GPT-2 small K = 8 and K = 12-16 gain 1-3 % too, and
-// fp32 K = 5-7 every mode 0-5 %.  At K = 4 the fused round gains 1 % but the
+// ahead); 3B K = 8 bf16, GPT-2 small K = 8 and K = 12-16 gain 1-3 % too, fp32
+// K = 5-7 every mode 0-5 %, bf16 K = 6-7 the fused round 2 % (3B).  At K = 4 the fused round gains 1 % but the
 // statistics-only mode and the update with statistics lose 3-9 % (the update
 // without them and the reset alone 10-23 %), and below K = 4 the
 // statistics-only mode needs more waves, so those keep 768.  Even multiples of
@@ -131,9 +131,9 @@ int blocks_for(const autoloco_ctx* ctx, int64_t n, int32_t dtype, int k, bool bf
     const int64_t nvec = n / v;
     int per_cu = (bf16p ? ctx->occupancy_bf16p : ctx->occupancy)[dtype == AUTOLOCO_BF16 ? 1 : 0][k];
     if (per_cu > 3) per_cu = 3;
-    // one workgroup per CU for the round's modes from K = 5 (fp32) or 8 (bf16
-    // replicas), where every mode is as fast or faster than at three
-    if (round_grid && k >= (dtype == AUTOLOCO_BF16 ? 8 : 5)) per_cu = 1;
+    // one workgroup per CU for the round's modes from K = 5 (fp32) or 6 (bf16
+    // replicas), where the modes are as fast or faster than at three
+    if (round_grid && k >= (dtype == AUTOLOCO_BF16 ? 6 : 5)) per_cu = 1;
     if (per_cu < 1) per_cu = 1;
     int limit = ctx->grid_limit > 0 ? ctx->grid_limit : ctx->num_cus * per_cu;
     if (limit > kMaxBlocks) limit = kMaxBlocks;

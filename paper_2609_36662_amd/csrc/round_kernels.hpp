@@ -159,7 +159,7 @@ __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K]
 }
 
 // Windows the statistics-only mode loads ahead: enough for about 512 bytes of
-// loads per lane (from K = 5 with fp32 replicas and from K = 8 with bf16 the
+// loads per lane (from K = 5 with fp32 replicas and from K = 6 with bf16 the
 // default grid holds one wave per SIMD), at most 8, within 200 registers for the
 // loaded words (below those K, whose grid keeps three workgroups per compute
 // unit, 100 with fp32 replicas and 64 with bf16, so that three waves per SIMD
@@ -169,7 +169,7 @@ template <int K, int RT>
 constexpr int stats_unroll() {
     const int words = RT == RT_F32 ? 4 * (K + 1) : 4 * K + 8;
     const int bytes = RT == RT_F32 ? 16 * (K + 1) : 32 + 16 * K;
-    const int cap = K >= (RT == RT_F32 ? 5 : 8) ? 200 : (RT == RT_F32 ? 100 : 64);
+    const int cap = K >= (RT == RT_F32 ? 5 : 6) ? 200 : (RT == RT_F32 ? 100 : 64);
     int u = (512 + bytes - 1) / bytes;
     if (u > 8) u = 8;
     while (u > 1 && u * words > cap) --u;
