@@ -124,10 +124,15 @@ __device__ __forceinline__ float tree_sum(const float (&d)[K]) {
 // BF16 (nearest even), their float64 sum in worker order times float64(1/K)
 // rounded to FP32, then to BF16 (its bits go to pb); the squared sums use the
 // unrounded Delta_k and that received mean.
+// Only the fused multiply-adds written out are fused: without the pragma the
+// compiler may fold the mean's product into Delta_k - mean in some kernel
+// variants and not in others, and the standalone and fused statistics would
+// then differ in their last bits.
 template <int K, bool STATS, bool UPDATE, bool BF16P>
 __device__ __forceinline__ void one_param(float th, float v, const float (&r)[K], const RoundArgs& a,
                                           float (&s)[K], float (&q)[K], float& m, float& th_new,
                                           float& v_new, uint32_t& pb) {
+#pragma clang fp contract(off)
     float d[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) d[k] = th - r[k];

@@ -131,8 +131,11 @@ def test_flag_subsets(ctx, flags):
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_standalone_stats_match_fused_bitwise(ctx, dtype):
-    n, k = 1_000_003, 8
+@pytest.mark.parametrize("k", [3, 5, 6, 8])
+def test_standalone_stats_match_fused_bitwise(ctx, dtype, k):
+    # every K on both sides of the grid thresholds (one workgroup per compute
+    # unit from K = 5 with fp32 replicas and from K = 6 with bf16)
+    n = 1_000_003
     inp = cpu_inputs(n, k, seed=11, replica_dtype=dtype)
     dev = to_device(inp)
     ref = _oracle_round(inp, _tiny_coeffs(False))
