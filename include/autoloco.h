@@ -297,12 +297,16 @@ int autoloco_traffic_reference(autoloco_ctx* ctx, const autoloco_buffers* bufs);
  *     the library instantiates are accepted (E_INVALID otherwise): with
  *     AUTOLOCO_PROBE_RUN1 (the fp32 round's window loop, one run of 4 elements
  *     per lane per window) 1, 2, 4, 6 or 10 streams in place, 1, 2, 4 or 10
- *     read, 1 or 10 written, 5 read and 5 written, 1 read and 1, 4, 8 or 16
+ *     read, 1 or 10 written, 5 read and 5 written, 1 read and 1, 2, 4, 8 or 16
  *     written; with AUTOLOCO_PROBE_RUN2 (two runs per lane, 256 runs apart: the
  *     bf16 round's and the per-GPU kernels' shape) 10 in place or read, one 4-byte read
  *     and 1, 4, 8 or 16 2-byte written, two 4-byte read (or one 4-byte and one
  *     2-byte) and one 2-byte written, two 4-byte in place with 1, 2, 4, 8 or 16
  *     2-byte read and one 2-byte written (or, for 4 and 8, none); with
+ *     AUTOLOCO_PROBE_RUN8 (eight runs per lane, 256 runs apart: 32 KB of every
+ *     4-byte stream per workgroup and window, the standalone reset's shape
+ *     with three or more fp32 replicas) 10 in place, read or written, and one
+ *     read and 4, 8 or 16 written; with
  *     AUTOLOCO_PROBE_SERIAL (every workgroup stages 16 KB of each read stream
  *     in LDS with direct loads, stream after stream, at most two streams'
  *     loads in flight, then stores stream by stream) and AUTOLOCO_PROBE_TILE
@@ -328,6 +332,7 @@ int autoloco_traffic_reference(autoloco_ctx* ctx, const autoloco_buffers* bufs);
 #define AUTOLOCO_PROBE_SERIAL 2
 #define AUTOLOCO_PROBE_TILE 3
 #define AUTOLOCO_PROBE_PHASED 4
+#define AUTOLOCO_PROBE_RUN8 5
 typedef struct {
     void* ptr;
     int32_t elem_bytes;

@@ -17,5 +17,5 @@ from ._lib import (  # noqa: F401
     lib, make_buffers, make_coeffs, make_observation, make_outer_cfg, make_schedule, spread_tensors,
     autoloco_inner_adamw, autoloco_last_adamw_ms, autoloco_adamw_traffic_reference, autoloco_rank_payload, autoloco_shard_step, make_adamw_buffers, make_adamw_coeffs,
     autoloco_traffic_reference, autoloco_traffic_probe, autoloco_build_id, autoloco_outer_step_static,
-    PROBE_READ, PROBE_WRITE, PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE, PROBE_PHASED,
+    PROBE_READ, PROBE_WRITE, PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE, PROBE_PHASED, PROBE_RUN8,
 )

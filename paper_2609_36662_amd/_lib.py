@@ -549,7 +549,7 @@ def autoloco_traffic_reference(ctx: Context, theta, momentum, replicas, n=None) 
 
 # -------------------------------------------------------- host scalars --
 PROBE_READ, PROBE_WRITE = 1, 2
-PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE, PROBE_PHASED = 0, 1, 2, 3, 4
+PROBE_RUN1, PROBE_RUN2, PROBE_SERIAL, PROBE_TILE, PROBE_PHASED, PROBE_RUN8 = 0, 1, 2, 3, 4, 5
 
 
 def autoloco_traffic_probe(ctx: Context, streams: Sequence, shape: int = PROBE_RUN1, blocks: int = 0,

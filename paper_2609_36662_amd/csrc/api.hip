@@ -801,7 +801,7 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
     if (c == nullptr) return AUTOLOCO_E_INVALID;
     if (streams == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null streams");
     if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
-    if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_PHASED)
+    if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_RUN8)
         return fail(c, AUTOLOCO_E_INVALID, "unknown probe shape");
     if (count < 1 || count > kProbeMaxStreams) return fail(c, AUTOLOCO_E_INVALID, "stream count outside 1..18");
     if (blocks < 0 || blocks > kMaxBlocks) return fail(c, AUTOLOCO_E_INVALID, "blocks outside 0..16384");
@@ -832,7 +832,7 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
     ProbePattern p;
     p.shape = shape == AUTOLOCO_PROBE_SERIAL ? PROBE_SERIAL : shape == AUTOLOCO_PROBE_TILE ? PROBE_TILE
             : shape == AUTOLOCO_PROBE_PHASED ? PROBE_PHASED : PROBE_RUN;
-    p.r = shape == AUTOLOCO_PROBE_RUN2 ? 2 : 1;
+    p.r = shape == AUTOLOCO_PROBE_RUN2 ? 2 : shape == AUTOLOCO_PROBE_RUN8 ? 8 : 1;
     p.a = cls_count[0];
     p.b = cls_count[1];
     p.c = cls_count[2];
@@ -1142,12 +1142,21 @@ int autoloco_last_adamw_ms(autoloco_ctx* c, float* norm_ms, float* update_ms) {
 // ------------------------------------------------------------ reset launcher
 namespace autoloco {
 namespace {
+// Windows of 256 quads per workgroup and iteration.  fp32 replicas: 8 from
+// three replicas on, where the longer contiguous writes per replica are 3-10 %
+// faster than one window on MI355X (1.1B: K = 8 6.20-6.28 ms against 6.64-6.85,
+// K = 6 4.83-4.88 against 5.37-5.53), one below (a copy at K = 1, which runs no
+// faster with longer spans).  bf16 replicas: two windows (a 4 KB run per
+// replica), faster than 4 to 16 at every K (3B, K = 8: 10.5 ms against 10.6-11.1;
+// K = 3: 5.1 against 5.5-6.1).
 template <int K>
 hipError_t reset_k(int rt, int blocks, hipStream_t s, const RoundArgs& a) {
     if (rt == RT_BF16)
-        hipLaunchKernelGGL((reset_kernel<K, RT_BF16>), dim3(blocks), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((reset_kernel<K, RT_BF16, 2>), dim3(blocks), dim3(kBlock), 0, s, a);
+    else if constexpr (K >= 3)
+        hipLaunchKernelGGL((reset_kernel<K, RT_F32, 8>), dim3(blocks), dim3(kBlock), 0, s, a);
     else
-        hipLaunchKernelGGL((reset_kernel<K, RT_F32>), dim3(blocks), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((reset_kernel<K, RT_F32, 1>), dim3(blocks), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 }  // namespace

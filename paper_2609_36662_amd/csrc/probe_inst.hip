@@ -14,7 +14,8 @@ struct ProbeEntry {
 };
 
 // the run shape: the ceiling table's patterns, then the traffic of the reset
-// (theta read, K replicas written: fp32, or bf16 with two runs per lane), of
+// (theta read, K replicas written: fp32 with one run per lane below three
+// replicas and eight from three on, or bf16 with two runs per lane), of
 // the worker payload (theta and the replica read, the payload written) and of
 // the shard step (theta and v in place, K payload shards read, the mean
 // written or not)
@@ -22,12 +23,14 @@ struct ProbeEntry {
     X(1, 10, 0, 0, 0, 0) X(1, 6, 0, 0, 0, 0) X(1, 4, 0, 0, 0, 0) X(1, 2, 0, 0, 0, 0) X(1, 1, 0, 0, 0, 0) \
     X(1, 0, 10, 0, 0, 0) X(1, 0, 8, 0, 0, 0) X(1, 0, 4, 0, 0, 0) X(1, 0, 2, 0, 0, 0) X(1, 0, 1, 0, 0, 0) \
     X(1, 0, 0, 0, 0, 10) X(1, 0, 0, 0, 0, 1) X(1, 0, 5, 0, 0, 5)                                         \
-    X(1, 0, 1, 0, 0, 1) X(1, 0, 1, 0, 0, 4) X(1, 0, 1, 0, 0, 8) X(1, 0, 1, 0, 0, 16)                     \
+    X(1, 0, 1, 0, 0, 1) X(1, 0, 1, 0, 0, 2) X(1, 0, 1, 0, 0, 4) X(1, 0, 1, 0, 0, 8) X(1, 0, 1, 0, 0, 16) \
     X(2, 10, 0, 0, 0, 0) X(2, 0, 10, 0, 0, 0)                                                          \
     X(2, 0, 1, 0, 1, 0) X(2, 0, 1, 0, 4, 0) X(2, 0, 1, 0, 8, 0) X(2, 0, 1, 0, 16, 0)                     \
     X(2, 0, 2, 0, 1, 0) X(2, 0, 1, 1, 1, 0)                                                            \
     X(2, 2, 0, 1, 1, 0) X(2, 2, 0, 2, 1, 0) X(2, 2, 0, 4, 1, 0) X(2, 2, 0, 8, 1, 0) X(2, 2, 0, 16, 1, 0) \
-    X(2, 2, 0, 4, 0, 0) X(2, 2, 0, 8, 0, 0)
+    X(2, 2, 0, 4, 0, 0) X(2, 2, 0, 8, 0, 0)                                                            \
+    X(8, 10, 0, 0, 0, 0) X(8, 0, 10, 0, 0, 0) X(8, 0, 0, 0, 0, 10)                                     \
+    X(8, 0, 1, 0, 0, 4) X(8, 0, 1, 0, 0, 8) X(8, 0, 1, 0, 0, 16)
 
 // the tile shapes: 10 streams in place, read, or written
 #define AUTOLOCO_PROBE_TILES(X) X(10, 0, 0) X(0, 10, 0) X(0, 0, 10)

@@ -19,8 +19,9 @@
 // Shapes:
 //   run      the round kernel's window loop: a lane owns R runs of 4 elements
 //            per window (R = 1: one run, the fp32 round's; R = 2: two runs 256
-//            apart, the bf16 round's and the per-GPU kernels'), at a 32-bit
-//            offset from a wave-uniform window base;
+//            apart, the bf16 round's and the per-GPU kernels'; R = 8: eight
+//            runs 256 apart, the standalone reset's with three or more fp32
+//            replicas), at a 32-bit offset from a wave-uniform window base;
 //   serial   a workgroup stages a tile of every read stream in LDS with direct
 //            global-to-LDS loads, stream after stream, waiting for stream s
 //            before it issues stream s + 2 (two streams' loads in flight per
@@ -75,12 +76,12 @@ __global__ void __launch_bounds__(kBlock) probe_run_kernel(ProbeArgs a) {
     uint32_t fold = 0;
     for (int64_t qb = (int64_t)blockIdx.x * kBlock * R; qb < nq; qb += qstride) {
         if (qb + threadIdx.x >= nq) continue;
-        const bool ok1 = R == 2 && qb + kBlock + threadIdx.x < nq;
+        const bool full = qb + (int64_t)kBlock * R <= nq;     // wave-uniform: every run in range
         u32x4 w4[N4 > 0 ? N4 : 1][R];
         u32x2r w2[C > 0 ? C : 1][R];
 #pragma unroll
         for (int h = 0; h < R; ++h) {
-            if (h == 1 && !ok1) continue;
+            if (h > 0 && !full && qb + h * kBlock + threadIdx.x >= nq) continue;
             const uint32_t run = h * kBlock + threadIdx.x;
 #pragma unroll
             for (int s = 0; s < N4; ++s) w4[s][h] = ld_u4_at(static_cast<const uint32_t*>(a.ptr[s]) + qb * 4, run * 16u);
@@ -90,7 +91,7 @@ __global__ void __launch_bounds__(kBlock) probe_run_kernel(ProbeArgs a) {
         }
 #pragma unroll
         for (int h = 0; h < R; ++h) {
-            if (h == 1 && !ok1) continue;
+            if (h > 0 && !full && qb + h * kBlock + threadIdx.x >= nq) continue;
             const uint32_t run = h * kBlock + threadIdx.x;
             const uint32_t x = (uint32_t)qb + run;
 #pragma unroll

@@ -8,37 +8,47 @@
 
 namespace autoloco {
 
-// theta_k <- theta for every replica.  The round kernel's window loop: a lane
-// owns one quad per window of 256 (fp32 replicas) or two, 256 quads apart
-// (bf16), at a 32-bit offset from a wave-uniform window base, so every load
-// and store instruction of a wavefront covers one contiguous run (1 KB of
-// theta, 1 KB of an fp32 replica, 512 B of a bf16 one).
+// Quad q of the span at element wb written into every replica.
 template <int K, int RT>
+__device__ __forceinline__ void store_quad(const RoundArgs& a, int64_t wb, uint32_t q, f32x4 t) {
+    if constexpr (RT == RT_F32) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, q * 16u, t);
+    } else {
+        const u32x2r w = {bf16_pack(t[0], t[1]), bf16_pack(t[2], t[3])};
+#pragma unroll
+        for (int k = 0; k < K; ++k) st_u2_at(static_cast<uint16_t*>(a.replicas[k]) + wb, q * 8u, w);   // bf16: 8 B a quad
+    }
+}
+
+// theta_k <- theta for every replica.  A workgroup takes U consecutive windows
+// of 256 quads of theta per iteration (U * 4 KB), loads them all, then writes
+// them into every replica, so that each replica receives one contiguous run of
+// U * 4 KB (fp32) or U * 2 KB (bf16) per workgroup and iteration.  A lane owns
+// quad u * 256 + lane of the span, at a 32-bit offset from the wave-uniform
+// span base, so every load and store instruction of a wavefront covers one
+// contiguous run (1 KB of theta, 1 KB of an fp32 replica, 512 B of a bf16 one).
+// The launcher picks U per replica type and K (longer runs pay off for
+// three or more fp32 replicas, whose writes dominate the traffic).
+template <int K, int RT, int U>
 __global__ void __launch_bounds__(kBlock) reset_kernel(RoundArgs a) {
-    constexpr int R = RT == RT_F32 ? 1 : 2;   // quads per lane per window
     const int64_t nq = a.n / 4;
-    const int64_t qstride = (int64_t)gridDim.x * kBlock * R;
+    constexpr int64_t span = (int64_t)kBlock * U;      // quads per workgroup and iteration
+    const int64_t qstride = (int64_t)gridDim.x * span;
     const int64_t gtid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (int64_t qb = (int64_t)blockIdx.x * kBlock * R; qb < nq; qb += qstride) {
-        if (qb + threadIdx.x >= nq) continue;
-        const bool ok1 = R == 2 && qb + kBlock + threadIdx.x < nq;
-        const int64_t wb = qb * 4;
-        if constexpr (RT == RT_F32) {
-            const uint32_t fo = threadIdx.x * 16u;
-            const f32x4 t = ld_f4_at(a.theta + wb, fo);
+    for (int64_t qb = (int64_t)blockIdx.x * span; qb < nq; qb += qstride) {
+        const int64_t wb = qb * 4;                     // element index of the span's first quad
+        if (qb + span <= nq) {                         // a whole span (wave-uniform): no per-lane test
+            f32x4 t[U];
 #pragma unroll
-            for (int k = 0; k < K; ++k) st_f4_at(static_cast<float*>(a.replicas[k]) + wb, fo, t);
-        } else {
-            f32x4 t[2] = {};
-            t[0] = ld_f4_at(a.theta + wb, threadIdx.x * 16u);
-            if (ok1) t[1] = ld_f4_at(a.theta + wb, (kBlock + threadIdx.x) * 16u);
+            for (int u = 0; u < U; ++u) t[u] = ld_f4_at(a.theta + wb, (u * kBlock + threadIdx.x) * 16u);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                if (h == 1 && !ok1) continue;
-                const uint32_t fo = (h * kBlock + threadIdx.x) * 8u;   // byte offset in bf16 buffers
-                const u32x2r w = {bf16_pack(t[h][0], t[h][1]), bf16_pack(t[h][2], t[h][3])};
+            for (int u = 0; u < U; ++u) store_quad<K, RT>(a, wb, u * kBlock + threadIdx.x, t[u]);
+        } else {                                       // the last, shorter span: quad by quad
 #pragma unroll
-                for (int k = 0; k < K; ++k) st_u2_at(static_cast<uint16_t*>(a.replicas[k]) + wb, fo, w);
+            for (int u = 0; u < U; ++u) {
+                const uint32_t q = u * kBlock + threadIdx.x;
+                if (qb + q < nq) store_quad<K, RT>(a, wb, q, ld_f4_at(a.theta + wb, q * 16u));
             }
         }
     }

@@ -234,12 +234,14 @@ def test_largest_grid(ctx, n, k):
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-@pytest.mark.parametrize("k", [1, 2, 8, 16])
+@pytest.mark.parametrize("k", [1, 2, 3, 8, 16])
 @pytest.mark.parametrize("n,grid", [(1, 0), (3, 0), (4 * 256 + 3, 0), (8 * 512 * 3 + 5, 3), (300_001, 0),
-                                    (300_001, 5)])
+                                    (300_001, 5), (8 * 1024 * 5 + 2 * 1024 + 7, 3), (8 * 1024 * 7 + 1, 2)])
 def test_broadcast_reset_shapes(ctx, dtype, k, n, grid):
     # the reset's window loop over ragged sizes, the last window shorter than one
-    # run per lane, and a capped grid that takes several grid-stride passes
+    # run per lane, a last span of fewer windows than a full one (8 windows of
+    # 1,024 elements from three fp32 replicas on), and a capped grid that takes
+    # several grid-stride passes
     inp = cpu_inputs(n, k, seed=23 + k, replica_dtype=dtype)
     dev = to_device(inp)
     al.autoloco_set_grid_limit(ctx, grid)

@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 
 R, W, RW = al.PROBE_READ, al.PROBE_WRITE, al.PROBE_READ | al.PROBE_WRITE
 TILE = 4 * 4 * 256          # elements of one tile per stream (4 runs of 4 per lane, 256 lanes)
-RUNS = (al.PROBE_RUN1, al.PROBE_RUN2)
+RUNS = (al.PROBE_RUN1, al.PROBE_RUN2, al.PROBE_RUN8)
 TILES = (al.PROBE_SERIAL, al.PROBE_TILE)
 
 
@@ -41,7 +41,7 @@ def _moved(shape, n):
     return n // TILE * TILE if shape in TILES else n // 4 * 4
 
 
-SIZES = [5, 4 * 256 + 3, 3 * TILE + 1000, 256 * 4 * 9 + 2]
+SIZES = [5, 4 * 256 + 3, 3 * TILE + 1000, 256 * 4 * 9 + 2, 8 * 1024 * 7 + 3 * 1024 + 3]
 
 
 @pytest.mark.parametrize("shape", RUNS + TILES)
@@ -59,12 +59,13 @@ def test_in_place_and_read_streams_keep_their_bits(ctx, shape, n, blocks, access
 
 
 @pytest.mark.parametrize("n", SIZES)
-@pytest.mark.parametrize("k", [1, 4, 8, 16])
-def test_written_streams_receive_stream_0(ctx, n, k):
+@pytest.mark.parametrize("shape,k", [(al.PROBE_RUN1, 1), (al.PROBE_RUN1, 2), (al.PROBE_RUN1, 4), (al.PROBE_RUN1, 8), (al.PROBE_RUN1, 16),
+                                     (al.PROBE_RUN8, 4), (al.PROBE_RUN8, 8), (al.PROBE_RUN8, 16)])
+def test_written_streams_receive_stream_0(ctx, n, shape, k):
     # the reset's pattern: theta read, k streams written with its words
     bufs = _bufs(n, k + 1, seed=3 * n + k)
     before = [_bits(b) for b in bufs]
-    moved = al.autoloco_traffic_probe(ctx, [(bufs[0], R)] + [(b, W) for b in bufs[1:]], al.PROBE_RUN1, 0)
+    moved = al.autoloco_traffic_probe(ctx, [(bufs[0], R)] + [(b, W) for b in bufs[1:]], shape, 3)
     torch.cuda.synchronize()
     per = n // 4 * 4
     for i in range(1, k + 1):
@@ -96,7 +97,7 @@ def test_two_byte_streams(ctx, n):
     assert moved == per * (2 * 4 * 2 + 8 * 2 + 2)
 
 
-@pytest.mark.parametrize("shape", [al.PROBE_RUN1, al.PROBE_TILE, al.PROBE_SERIAL])
+@pytest.mark.parametrize("shape", [al.PROBE_RUN1, al.PROBE_RUN8, al.PROBE_TILE, al.PROBE_SERIAL])
 def test_pure_write_writes_run_index(ctx, shape):
     n = 3 * TILE + 7
     bufs = _bufs(n, 10, seed=5)
@@ -118,6 +119,7 @@ def test_bad_arguments_launch_nothing(ctx):
         ([(bufs[0], W), (bufs[1], R)], al.PROBE_RUN1, 0),            # classes out of order
         ([(half[0], RW)], al.PROBE_RUN2, 0),                         # 2-byte stream in place
         ([(bufs[0], 0)], al.PROBE_RUN1, 0),                          # no access
+        ([(bufs[0], R), (bufs[1], W)], al.PROBE_RUN8, 0),            # 1 read, 1 written: not at 8 runs
         ([(bufs[0], RW)], 7, 0),                                     # unknown shape
         ([(bufs[0], RW)], al.PROBE_RUN1, 20000),                     # too many workgroups
     ]
