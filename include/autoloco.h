@@ -140,10 +140,12 @@ int autoloco_free(autoloco_ctx* ctx, void* ptr);
 
 /* Every buffer argument of the device calls below must be device (or managed)
  * memory of the context's device; host memory and memory of another device are
- * rejected with E_INVALID before anything is launched. */
+ * rejected with E_INVALID before anything is launched.  Element counts n lie in
+ * 0..2^56 (E_INVALID otherwise), so no byte count or address the library forms
+ * from them overflows. */
 
 typedef struct {
-    int64_t n;             /* parameters per buffer, n >= 0 */
+    int64_t n;             /* parameters per buffer, 0 <= n <= 2^56 */
     int32_t k;             /* worker replicas, 1..AUTOLOCO_MAX_K */
     int32_t replica_dtype; /* autoloco_dtype of every replica */
     float* theta;          /* [n] fp32: synchronised parameters theta_t (in/out) */
@@ -440,7 +442,7 @@ typedef struct {
  * Element arithmetic is fp32 with the step's scalars rounded once to fp32.
  * A non-finite gradient is not an error: it propagates into the state and
  * finite = 0.
- * Errors: E_INVALID (k outside 1..16, n < 0, null buffer, partial model_bf16,
+ * Errors: E_INVALID (k outside 1..16, n outside 0..2^56, null buffer, partial model_bf16,
  * step < 1, lr / eps / weight_decay / max_grad_norm negative or not finite,
  * beta outside [0, 1)), E_ALIGN, E_ALIAS, E_DEVICE. */
 int autoloco_inner_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* bufs,

@@ -159,12 +159,17 @@ struct Range {
     const char* name;
 };
 
+// Largest element count a call accepts: far beyond any device's memory, small
+// enough that no byte count or address computed from it overflows.
+constexpr int64_t kMaxN = int64_t(1) << 56;
+const char* const kBadN = "n outside 0..2^56";
+
 // Checks pointers, sizes, alignment and overlap.  need_momentum: the call
 // reads and writes the momentum buffer.
 int validate(autoloco_ctx* ctx, const autoloco_buffers* b, bool need_momentum) {
     if (ctx == nullptr) return AUTOLOCO_E_INVALID;
     if (b == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null buffers");
-    if (b->n < 0) return fail(ctx, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->n < 0 || b->n > kMaxN) return fail(ctx, AUTOLOCO_E_INVALID, kBadN);
     if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(ctx, AUTOLOCO_E_INVALID, "k outside 1..16");
     if (b->replica_dtype != AUTOLOCO_F32 && b->replica_dtype != AUTOLOCO_BF16)
         return fail(ctx, AUTOLOCO_E_INVALID, "unknown replica dtype");
@@ -305,7 +310,7 @@ int run_round(autoloco_ctx* ctx, const autoloco_buffers* b, const RoundArgs& a, 
 int validate_adamw(autoloco_ctx* ctx, const autoloco_adamw_buffers* b, bool* copy) {
     if (ctx == nullptr) return AUTOLOCO_E_INVALID;
     if (b == nullptr) return fail(ctx, AUTOLOCO_E_INVALID, "null buffers");
-    if (b->n < 0) return fail(ctx, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->n < 0 || b->n > kMaxN) return fail(ctx, AUTOLOCO_E_INVALID, kBadN);
     if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(ctx, AUTOLOCO_E_INVALID, "k outside 1..16");
     int ncopy = 0;
     for (int k = 0; k < b->k; ++k) ncopy += b->model_bf16[k] != nullptr;
@@ -612,7 +617,7 @@ int autoloco_set_grid_limit(autoloco_ctx* c, int max_blocks) {
 
 int autoloco_launch_shape(const autoloco_ctx* c, int64_t n, int32_t k, int32_t dtype, int32_t* blocks,
                           int32_t* threads) {
-    if (c == nullptr || blocks == nullptr || threads == nullptr || n < 0) return AUTOLOCO_E_INVALID;
+    if (c == nullptr || blocks == nullptr || threads == nullptr || n < 0 || n > kMaxN) return AUTOLOCO_E_INVALID;
     if (dtype != AUTOLOCO_F32 && dtype != AUTOLOCO_BF16) return AUTOLOCO_E_INVALID;
     if (k < 1 || k > AUTOLOCO_MAX_K) return AUTOLOCO_E_INVALID;
     *blocks = blocks_for(c, n, dtype, k);
@@ -800,7 +805,7 @@ int autoloco_traffic_probe(autoloco_ctx* c, int64_t n, const autoloco_probe_stre
                            int32_t shape, int32_t blocks, double* bytes) {
     if (c == nullptr) return AUTOLOCO_E_INVALID;
     if (streams == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null streams");
-    if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (n < 0 || n > kMaxN) return fail(c, AUTOLOCO_E_INVALID, kBadN);
     if (shape < AUTOLOCO_PROBE_RUN1 || shape > AUTOLOCO_PROBE_RUN8)
         return fail(c, AUTOLOCO_E_INVALID, "unknown probe shape");
     if (count < 1 || count > kProbeMaxStreams) return fail(c, AUTOLOCO_E_INVALID, "stream count outside 1..18");
@@ -954,7 +959,7 @@ int autoloco_free(autoloco_ctx* c, void* ptr) {
 int autoloco_rank_payload(autoloco_ctx* c, int64_t n, const float* theta, const void* replica, int32_t dtype,
                           uint16_t* payload, double* sq_norm) {
     if (c == nullptr) return AUTOLOCO_E_INVALID;
-    if (n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (n < 0 || n > kMaxN) return fail(c, AUTOLOCO_E_INVALID, kBadN);
     if (dtype != AUTOLOCO_F32 && dtype != AUTOLOCO_BF16) return fail(c, AUTOLOCO_E_INVALID, "unknown replica dtype");
     if (n == 0) {
         if (sq_norm != nullptr) *sq_norm = 0.0;
@@ -985,7 +990,7 @@ int autoloco_shard_step(autoloco_ctx* c, const autoloco_shard_buffers* b, const 
                         uint16_t* mean_bf16, double* sq_mean) {
     if (c == nullptr) return AUTOLOCO_E_INVALID;
     if (b == nullptr || co == nullptr) return fail(c, AUTOLOCO_E_INVALID, "null buffers or coefficients");
-    if (b->n < 0) return fail(c, AUTOLOCO_E_INVALID, "n < 0");
+    if (b->n < 0 || b->n > kMaxN) return fail(c, AUTOLOCO_E_INVALID, kBadN);
     if (b->k < 1 || b->k > AUTOLOCO_MAX_K) return fail(c, AUTOLOCO_E_INVALID, "k outside 1..16");
     const int cs = check_coeffs(c, co);
     if (cs != AUTOLOCO_OK) return cs;

@@ -364,6 +364,8 @@ def test_rejects_bad_arguments_without_touching_buffers(ctx):
     assert _raw(ctx, th, mo, [r0, r1], n, 2, dtype=7) == -1       # unknown dtype
     assert _raw(ctx, th, mo, [r0, r1], n, 2, flags=4) == -1       # unknown flag
     assert _raw(ctx, th, mo, [r0, r1], -1, 2) == -1               # negative n
+    assert _raw(ctx, th, mo, [r0, r1], 2**56 + 1, 2) == -1        # n beyond 2^56
+    assert "2^56" in al.autoloco_last_error(ctx)
     for bad_eps in (0.0, -1e-12, float("nan"), float("inf")):    # eps > 0 (eq. adaptive-h-core-diagnostics)
         assert _raw(ctx, th, mo, [r0, r1], n, 2, eps=bad_eps) == -1
     assert al.autoloco_last_error(ctx)                            # a message was left
