@@ -47,54 +47,62 @@ struct ShardArgs {
 // base, so every wavefront instruction covers one contiguous run (1 KB of fp32,
 // 512 B of bf16) and no cache line is written in parts.  The last n mod 4
 // parameters go to threads of workgroup 0.
+// One window of rank_payload_kernel for one lane: its two quads (FULL: both in
+// range, a wave-uniform fact; else only those below `left` quads from the
+// window's start), both loaded before any store (the payload store could alias
+// the inputs as far as the compiler knows, so it would not move a later load
+// above it).  Returns the lane's fp32 sum of squares over the window.
+template <int RT, bool FULL>
+__device__ __forceinline__ float payload_window(const RankPayloadArgs& a, int64_t wb, int64_t left) {
+    f32x4 t[2], r4[2];
+    u32x2r rw[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t run = h * kBlock + threadIdx.x;
+        if (!FULL && run >= left) continue;
+        t[h] = ld_f4_at(a.theta + wb, run * 16u);
+        if constexpr (RT == RT_F32)
+            r4[h] = ld_f4_at(static_cast<const float*>(a.replica) + wb, run * 16u);
+        else
+            rw[h] = ld_u2_at(static_cast<const uint16_t*>(a.replica) + wb, run * 8u);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t run = h * kBlock + threadIdx.x;
+        if (!FULL && run >= left) continue;
+        float r[4];
+        if constexpr (RT == RT_F32) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) r[e] = r4[h][e];
+        } else {
+            r[0] = bf16_lo(rw[h][0]);
+            r[1] = bf16_hi(rw[h][0]);
+            r[2] = bf16_lo(rw[h][1]);
+            r[3] = bf16_hi(rw[h][1]);
+        }
+        float d[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            d[e] = t[h][e] - r[e];
+            s = __builtin_fmaf(d[e], d[e], s);
+        }
+        st_u2_at(a.payload + wb, run * 8u, u32x2r{bf16_pack(d[0], d[1]), bf16_pack(d[2], d[3])});
+    }
+    return s;
+}
+
 template <int RT>
 __global__ void __launch_bounds__(kBlock) rank_payload_kernel(RankPayloadArgs a) {
     double acc[1] = {0.0};
     const int64_t nq = a.n / 4;
     const int64_t stride = (int64_t)gridDim.x * kBlock * 2;
     for (int64_t qb = (int64_t)blockIdx.x * kBlock * 2; qb < nq; qb += stride) {
-        if (qb + threadIdx.x >= nq) continue;
-        const bool ok1 = qb + kBlock + threadIdx.x < nq;
         const int64_t wb = qb * 4;                       // first parameter of the window
-        // both runs' loads before any store: the payload store could alias the
-        // inputs as far as the compiler knows, so it would not move a later
-        // load above it
-        f32x4 t[2] = {}, r4[2] = {};
-        u32x2r rw[2] = {};
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (h == 1 && !ok1) continue;
-            const uint32_t run = h * kBlock + threadIdx.x;
-            t[h] = ld_f4_at(a.theta + wb, run * 16u);
-            if constexpr (RT == RT_F32)
-                r4[h] = ld_f4_at(static_cast<const float*>(a.replica) + wb, run * 16u);
-            else
-                rw[h] = ld_u2_at(static_cast<const uint16_t*>(a.replica) + wb, run * 8u);
-        }
-        float s = 0.f;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (h == 1 && !ok1) continue;
-            const uint32_t run = h * kBlock + threadIdx.x;
-            float r[4];
-            if constexpr (RT == RT_F32) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) r[e] = r4[h][e];
-            } else {
-                r[0] = bf16_lo(rw[h][0]);
-                r[1] = bf16_hi(rw[h][0]);
-                r[2] = bf16_lo(rw[h][1]);
-                r[3] = bf16_hi(rw[h][1]);
-            }
-            float d[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                d[e] = t[h][e] - r[e];
-                s = __builtin_fmaf(d[e], d[e], s);
-            }
-            st_u2_at(a.payload + wb, run * 8u, u32x2r{bf16_pack(d[0], d[1]), bf16_pack(d[2], d[3])});
-        }
-        acc[0] += (double)s;
+        if (qb + 2 * kBlock <= nq)                       // a whole window: no per-lane test
+            acc[0] += (double)payload_window<RT, true>(a, wb, 0);
+        else if (qb + threadIdx.x < nq)                  // the last, shorter window
+            acc[0] += (double)payload_window<RT, false>(a, wb, nq - qb);
     }
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3)) {
         const int64_t j = nq * 4 + threadIdx.x;
@@ -126,48 +134,55 @@ __device__ __forceinline__ float shard_one(const ShardArgs& a, const float (&b)[
     return mean;
 }
 
+// One window of shard_step_kernel for one lane (FULL and left as in
+// payload_window); returns the lane's fp32 sum of the squared means.
+template <int K, bool FULL>
+__device__ __forceinline__ float shard_window(const ShardArgs& a, int64_t wb, int64_t left) {
+    f32x4 t4[2], v4[2];
+    u32x2r w[K][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t run = h * kBlock + threadIdx.x;
+        if (!FULL && run >= left) continue;
+        t4[h] = ld_f4_at(a.theta + wb, run * 16u);
+        v4[h] = ld_f4_at(a.momentum + wb, run * 16u);
+#pragma unroll
+        for (int k = 0; k < K; ++k) w[k][h] = ld_u2_at(a.payloads[k] + wb, run * 8u);
+    }
+    float m = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t run = h * kBlock + threadIdx.x;
+        if (!FULL && run >= left) continue;
+        float th_new[4], v_new[4];
+        uint32_t pb[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float be[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) be[k] = (e & 1) ? bf16_hi(w[k][h][e >> 1]) : bf16_lo(w[k][h][e >> 1]);
+            const float mean = shard_one<K>(a, be, t4[h][e], v4[h][e], th_new[e], v_new[e], pb[e]);
+            m = __builtin_fmaf(mean, mean, m);
+        }
+        st_f4_at(a.theta + wb, run * 16u, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
+        st_f4_at(a.momentum + wb, run * 16u, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
+        if (a.mean_out != nullptr)
+            st_u2_at(a.mean_out + wb, run * 8u, u32x2r{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16});
+    }
+    return m;
+}
+
 template <int K>
 __global__ void __launch_bounds__(kBlock) shard_step_kernel(ShardArgs a) {
     double acc[1] = {0.0};
     const int64_t nq = a.n / 4;
     const int64_t stride = (int64_t)gridDim.x * kBlock * 2;
     for (int64_t qb = (int64_t)blockIdx.x * kBlock * 2; qb < nq; qb += stride) {
-        if (qb + threadIdx.x >= nq) continue;
-        const bool ok1 = qb + kBlock + threadIdx.x < nq;
         const int64_t wb = qb * 4;                       // first parameter of the window
-        // both runs' loads before any store (see rank_payload_kernel)
-        f32x4 t4[2] = {}, v4[2] = {};
-        u32x2r w[K][2] = {};
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (h == 1 && !ok1) continue;
-            const uint32_t run = h * kBlock + threadIdx.x;
-            t4[h] = ld_f4_at(a.theta + wb, run * 16u);
-            v4[h] = ld_f4_at(a.momentum + wb, run * 16u);
-#pragma unroll
-            for (int k = 0; k < K; ++k) w[k][h] = ld_u2_at(a.payloads[k] + wb, run * 8u);
-        }
-        float m = 0.f;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (h == 1 && !ok1) continue;
-            const uint32_t run = h * kBlock + threadIdx.x;
-            float th_new[4], v_new[4];
-            uint32_t pb[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float be[K];
-#pragma unroll
-                for (int k = 0; k < K; ++k) be[k] = (e & 1) ? bf16_hi(w[k][h][e >> 1]) : bf16_lo(w[k][h][e >> 1]);
-                const float mean = shard_one<K>(a, be, t4[h][e], v4[h][e], th_new[e], v_new[e], pb[e]);
-                m = __builtin_fmaf(mean, mean, m);
-            }
-            st_f4_at(a.theta + wb, run * 16u, f32x4{th_new[0], th_new[1], th_new[2], th_new[3]});
-            st_f4_at(a.momentum + wb, run * 16u, f32x4{v_new[0], v_new[1], v_new[2], v_new[3]});
-            if (a.mean_out != nullptr)
-                st_u2_at(a.mean_out + wb, run * 8u, u32x2r{pb[0] | pb[1] << 16, pb[2] | pb[3] << 16});
-        }
-        acc[0] += (double)m;
+        if (qb + 2 * kBlock <= nq)                       // a whole window: no per-lane test
+            acc[0] += (double)shard_window<K, true>(a, wb, 0);
+        else if (qb + threadIdx.x < nq)                  // the last, shorter window
+            acc[0] += (double)shard_window<K, false>(a, wb, nq - qb);
     }
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3)) {
         const int64_t j = nq * 4 + threadIdx.x;
