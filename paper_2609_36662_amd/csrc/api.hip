@@ -115,11 +115,11 @@ int check_device_ptr(autoloco_ctx* ctx, uintptr_t p, const char* name) {
 // 256 workgroups against 14.37-14.57 at 768 (the traffic reference alike), and
 // no mode slower (statistics only 6.28 against 6.37 ms, with its windows loaded
 // ahead); 3B K = 8 bf16, GPT-2 small K = 8 and K = 12-16 gain 1-3 % too, fp32
-// K = 5-7 every mode 0-5 %, bf16 K = 6-7 the fused round 2 % (3B).  At K = 4 the fused round gains 1 % but the
-// statistics-only mode and the update with statistics lose 3-9 % (the update
-// without them and the reset alone 10-23 %), and below K = 4 the
-// statistics-only mode needs more waves, so those keep 768.  Even multiples of
-// 256 are the slowest.  Every mode of a given (k, replica type) uses the same
+// K = 5-7 every mode 0-5 %, bf16 K = 6-7 the fused round by 2 % (3B).  At K = 4
+// the fused round gains 1 % but the statistics-only mode and the update with
+// statistics lose 3-9 % (the update without them and the reset alone 10-23 %),
+// and below K = 4 the statistics-only mode needs more waves, so those keep 768.
+// Even multiples of 256 are the slowest.  Every mode of a given (k, replica type) uses the same
 // grid, so the statistics of a standalone and of a fused call are summed in the
 // same order, bit for bit.
 // round_grid = false: a kernel with no statistics to keep in step with the
